@@ -1,0 +1,224 @@
+"""Seeded synthetic inputs shaped like the Wan-class video-latent workloads.
+
+This module only draws inputs: Q, K, V for one or more requests, the
+cross-request perturbations, and the fixed random mask of the tiny check.  It
+holds none of the method's arithmetic (no pooling, scoring, selection,
+quantisation or attention), so the HIP path and the CPU oracle can both read
+its output without sharing any computation.
+
+Recipe (the paper's own latents are not available; these stand in for the
+Wan2.2 self-attention inputs of Sec. 4.1):
+
+* Tokens sit on a (T, Y, X) latent grid in frame-major raster order,
+  n = (t * Y + y) * X + x.
+* 16 sinusoidal position features: sin and cos of 2*pi*c/P for the 8
+  (axis, period) pairs t:{2T, T}, y:{2Y, Y, Y/2}, x:{2X, X, X/2}.
+* Head h uses one projection W_h ~ N(0, (gamma_h / 4)^2) of shape [16, D]
+  shared by Q and K, gamma_h = 0.6 + 0.4 h / (H - 1), so q.k is a positional
+  locality kernel whose sharpness differs per head (the per-head sparsity
+  spread the paper schedules around in Sec. 3.2).
+* Q = f W_h + 0.5 eps_Q, K = f W_h + 0.5 eps_K, V ~ N(0, 1).
+* Cross-request inputs: a base request (seed s) and requests r = 0, 1, ...
+  (seed s + 1 + r) with Q_r = Q_base + 0.3 n_Q, K_r = K_base + 0.3 n_K and a
+  fresh V_r -- similar requests in the sense of Sec. 3.2, Obs. 1.
+* Every (seed, head) pair draws from its own PCG64 stream seeded by
+  SeedSequence([seed, h]) in the order W, eps_Q, eps_K, V (base requests draw
+  W, eps_Q, eps_K only; perturbed requests draw n_Q, n_K, V).  Values are
+  produced in float32 and rounded once (round-to-nearest-even) to the storage
+  dtype; both sides read those stored values.
+"""
+
+from __future__ import annotations
+
+import math
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+BLOCK = 64
+HEAD_DIM = 128
+
+
+@dataclass(frozen=True)
+class Workload:
+    key: str
+    dtype: str            # storage / compute type of the attention: "f16", "bf16", "fp8"
+    B: int
+    H: int
+    grid: tuple           # (T, Y, X)
+    density: float        # target kept fraction of (q-block, kv-block) pairs
+    mask_source: str      # "random" | "self" | "historical" | "request0"
+    seed: int
+    top_p: float = 0.0    # frozen calibration (joint top-p / top-k mode)
+    min_top_k: float = 0.0
+    D: int = HEAD_DIM
+
+    @property
+    def S(self) -> int:
+        T, Y, X = self.grid
+        return T * Y * X
+
+    @property
+    def n_blocks(self) -> int:
+        return (self.S + BLOCK - 1) // BLOCK
+
+    @property
+    def sm_scale(self) -> float:
+        return 1.0 / math.sqrt(self.D)
+
+    @property
+    def storage_dtype(self) -> torch.dtype:
+        return torch.float16 if self.dtype == "f16" else torch.bfloat16
+
+
+# top_p values are frozen outputs of oracle/calibrate_top_p.py: the oracle
+# builder's mean density is bisected onto the target with min_top_k =
+# density / 4 (achieved: 0.20153, 0.15074, 0.09834, 0.15145).
+WORKLOADS = {
+    "tiny_f16": Workload("tiny_f16", "f16", 1, 2, (4, 32, 32), 0.25, "random", 25040),
+    "wan5b_720p_bf16": Workload("wan5b_720p_bf16", "bf16", 1, 24, (31, 22, 40), 0.20, "self",
+                                25140, top_p=0.4814321762369126, min_top_k=0.05),
+    "wan14b_480p_reuse_bf16": Workload("wan14b_480p_reuse_bf16", "bf16", 1, 40, (21, 30, 52),
+                                       0.15, "historical", 25240, top_p=0.4067496571495548,
+                                       min_top_k=0.0375),
+    "wan14b_720p_fp8": Workload("wan14b_720p_fp8", "fp8", 1, 40, (21, 45, 80), 0.10, "self",
+                                25340, top_p=0.3092847240125824, min_top_k=0.025),
+    "wan14b_480p_batch4_bf16": Workload("wan14b_480p_batch4_bf16", "bf16", 4, 40, (21, 30, 52),
+                                        0.15, "request0", 25440, top_p=0.4150746473110233,
+                                        min_top_k=0.0375),
+}
+ORDER = ["tiny_f16", "wan5b_720p_bf16", "wan14b_480p_reuse_bf16", "wan14b_720p_fp8",
+         "wan14b_480p_batch4_bf16"]
+
+
+def position_features(grid) -> np.ndarray:
+    """[S, 16] float64 sinusoidal (t, y, x) features."""
+    T, Y, X = grid
+    n = np.arange(T * Y * X)
+    t = n // (Y * X)
+    y = (n // X) % Y
+    x = n % X
+    pairs = [(t, 2 * T), (t, T), (y, 2 * Y), (y, Y), (y, Y / 2), (x, 2 * X), (x, X), (x, X / 2)]
+    cols = []
+    for c, P in pairs:
+        ang = 2.0 * np.pi * c / P
+        cols.append(np.sin(ang))
+        cols.append(np.cos(ang))
+    return np.stack(cols, axis=1)
+
+
+def head_gamma(h: int, H: int) -> float:
+    return 0.6 + (0.4 * h / (H - 1) if H > 1 else 0.0)
+
+
+def _stream(seed: int, h: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, h])))
+
+
+def _base_qk(f: np.ndarray, seed: int, h: int, H: int, D: int):
+    g = _stream(seed, h)
+    W = g.standard_normal((16, D)) * (head_gamma(h, H) / 4.0)
+    loc = (f @ W).astype(np.float32)
+    S = f.shape[0]
+    q = loc + np.float32(0.5) * g.standard_normal((S, D), dtype=np.float32)
+    k = loc + np.float32(0.5) * g.standard_normal((S, D), dtype=np.float32)
+    return q, k, g
+
+
+def _threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+@dataclass
+class Inputs:
+    """Host tensors ``[B, S, H, D]`` in the storage dtype (bf16 for fp8 workloads)."""
+    q: torch.Tensor
+    k: torch.Tensor
+    v: torch.Tensor
+    mask_q: torch.Tensor | None      # request(s) the mask is built from, [Bm, S, H, D]
+    mask_k: torch.Tensor | None
+    random_mask: tuple | None        # (row_ptr, col_idx) int32 numpy, for "random"
+
+
+def make_inputs(wl: Workload, with_v: bool = True) -> Inputs:
+    S, H, D, B = wl.S, wl.H, wl.D, wl.B
+    dt = wl.storage_dtype
+    f = position_features(wl.grid)
+    q = torch.empty((B, S, H, D), dtype=dt)
+    k = torch.empty((B, S, H, D), dtype=dt)
+    v = torch.empty((B, S, H, D), dtype=dt) if with_v else None
+    hist_q = hist_k = None
+    perturbed = wl.mask_source in ("historical", "request0")
+    if wl.mask_source == "historical":
+        hist_q = torch.empty((1, S, H, D), dtype=dt)
+        hist_k = torch.empty((1, S, H, D), dtype=dt)
+
+    def head(h: int):
+        bq, bk, g = _base_qk(f, wl.seed, h, H, D)
+        if not perturbed:
+            # the request itself is drawn from (seed, h): W, eps_Q, eps_K, V
+            q[0, :, h, :].copy_(torch.from_numpy(bq))
+            k[0, :, h, :].copy_(torch.from_numpy(bk))
+            if with_v:
+                v[0, :, h, :].copy_(torch.from_numpy(g.standard_normal((S, D), dtype=np.float32)))
+            return
+        if hist_q is not None:
+            hist_q[0, :, h, :].copy_(torch.from_numpy(bq))
+            hist_k[0, :, h, :].copy_(torch.from_numpy(bk))
+        for b in range(B):
+            gr = _stream(wl.seed + 1 + b, h)
+            nq = gr.standard_normal((S, D), dtype=np.float32)
+            nk = gr.standard_normal((S, D), dtype=np.float32)
+            q[b, :, h, :].copy_(torch.from_numpy(bq + np.float32(0.3) * nq))
+            k[b, :, h, :].copy_(torch.from_numpy(bk + np.float32(0.3) * nk))
+            if with_v:
+                v[b, :, h, :].copy_(torch.from_numpy(gr.standard_normal((S, D), dtype=np.float32)))
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(head, range(H)))
+
+    if wl.mask_source == "random":
+        return Inputs(q, k, v, None, None, random_mask(wl))
+    if wl.mask_source == "historical":
+        return Inputs(q, k, v, hist_q, hist_k, None)
+    if wl.mask_source == "request0":
+        return Inputs(q, k, v, q[0:1], k[0:1], None)
+    return Inputs(q, k, v, q, k, None)
+
+
+def random_mask(wl: Workload, keep: int | None = None):
+    """Fixed random block mask of the tiny check: per (head, q-block) row the
+    diagonal block plus ``keep - 1`` distinct others drawn without replacement,
+    ascending.  Rows are ordered (h, i); one mask shared by the batch."""
+    n = wl.n_blocks
+    keep = int(round(wl.density * n)) if keep is None else keep
+    rng = np.random.Generator(np.random.PCG64(wl.seed + 7))
+    rows = []
+    for h in range(wl.H):
+        for i in range(n):
+            others = np.array([j for j in range(n) if j != i])
+            pick = rng.choice(others, keep - 1, replace=False)
+            rows.append(np.sort(np.concatenate([[i], pick])))
+    counts = np.array([len(r) for r in rows])
+    row_ptr = np.zeros(len(rows) + 1, dtype=np.int32)
+    np.cumsum(counts, out=row_ptr[1:])
+    return row_ptr, np.concatenate(rows).astype(np.int32)
+
+
+def random_csr(rng: np.random.Generator, rows: int, n: int, p_keep: float, empty_frac: float = 0.0):
+    """Random ascending CSR rows for fuzz tests (may include empty rows)."""
+    out = []
+    for _ in range(rows):
+        if rng.random() < empty_frac:
+            out.append(np.zeros(0, dtype=np.int32))
+            continue
+        sel = np.nonzero(rng.random(n) < p_keep)[0]
+        out.append(sel.astype(np.int32))
+    counts = np.array([len(r) for r in out], dtype=np.int64)
+    row_ptr = np.zeros(rows + 1, dtype=np.int32)
+    np.cumsum(counts, out=row_ptr[1:])
+    col = np.concatenate(out).astype(np.int32) if counts.sum() else np.zeros(0, np.int32)
+    return row_ptr, col
