@@ -1,0 +1,252 @@
+/*
+ * chorus.h -- C ABI of libchorus.so: block-sparse self-attention driven by a
+ * reusable block mask, for AMD Instinct MI355X (gfx950).
+ *
+ * Method: Chorus II, "Cross-Request Sparsity Reuse for Efficient
+ * Image-to-Video Generation".  A block mask is built once (for a historical
+ * request, Sec. 3.2 "Mask Caching and Retrieval") and then loaded and applied
+ * as-is to the block-sparse attention of new, similar requests (same passage;
+ * Sec. 3.2 Obs. 1).  This library provides the two pieces of that hot path:
+ *
+ *   - the mask builder: mean-pooled block scores softmax(mean(Q) mean(K)^T)
+ *     (Sec. 3.2 Obs. 2, the online predictor used on a cache miss) with joint
+ *     top-p / minimum-top-k selection (Sec. 3.2 "Mask Caching and Retrieval",
+ *     "Minimum top-k guarantee"; knobs top_p / min_top_k in Sec. 4.1);
+ *   - the block-sparse attention forward pass that evaluates only the listed
+ *     block pairs in QK^T, softmax and PV (Sec. 3.2 "Efficient block-sparse
+ *     kernel"), in fp16/bf16 and in FP8 with fp32 accumulation.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers on the current HIP device and are
+ *    owned by the caller.  The library never allocates, frees or synchronises;
+ *    every kernel is enqueued on `stream` (a hipStream_t, NULL = default).
+ *  - Q, K, V and outputs are [B, S, H, D] tensors: B requests, S tokens,
+ *    H heads, head dim D contiguous (the layout the paper indexes as
+ *    K[:, 0:N0, :, :] in Eq. (1)).  Strides are in elements; every token row
+ *    (D elements) must start 16-byte aligned.  D must be 128.
+ *  - Tokens are grouped in blocks of 64 (the mask granularity); n_blocks =
+ *    ceil(S / 64).  A partial last block is handled inside the kernels (no
+ *    padding is required in memory): keys at or beyond S carry no weight,
+ *    output rows at or beyond S do not exist.
+ *  - A block mask is CSR over rows r = (b_m * H + h) * n_blocks + i for mask
+ *    request b_m, head h and query block i; row r lists the kv blocks that
+ *    q-block i attends to, strictly ascending.  mask_batch == B gives one mask
+ *    per request; mask_batch == 1 reuses one mask for every request (the
+ *    cross-request reuse the paper is about).
+ *  - Functions return chorus_status.  Arguments are validated on the host
+ *    before anything is launched; on error nothing is enqueued and
+ *    chorus_last_error() (thread-local) describes the problem.  Launch
+ *    failures map to CHORUS_ERR_HIP.  Kernels trust a mask that passed the
+ *    host checks; chorus_validate_block_mask checks its contents on device.
+ */
+#ifndef CHORUS_H_
+#define CHORUS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CHORUS_OK = 0,
+  CHORUS_ERR_INVALID_ARG = 1,  /* null pointer, bad shape/stride/alignment, bad knob   */
+  CHORUS_ERR_UNSUPPORTED = 2,  /* D != 128, block != 64, too many blocks, bad dtype    */
+  CHORUS_ERR_CAPACITY = 3,     /* col_idx capacity below the worst case               */
+  CHORUS_ERR_HIP = 4,          /* a HIP launch or runtime call failed                 */
+  CHORUS_ERR_WORKSPACE = 5     /* workspace missing or smaller than the queried size  */
+} chorus_status;
+
+typedef enum {
+  CHORUS_F16 = 0,      /* IEEE binary16                                   */
+  CHORUS_BF16 = 1,     /* bfloat16                                        */
+  CHORUS_FP8_E4M3 = 2  /* OCP FP8 e4m3fn codes (uint8) + fp32 block scales */
+} chorus_dtype;
+
+/* Problem shape shared by the tensors of one call. */
+typedef struct {
+  int32_t B;  /* requests (batch)                     */
+  int32_t S;  /* tokens per request, >= 1              */
+  int32_t H;  /* heads                                 */
+  int32_t D;  /* head dim; must be 128                 */
+} chorus_shape;
+
+/* One [B, S, H, D] tensor: base pointer and element strides (D contiguous). */
+typedef struct {
+  void* data;
+  int64_t stride_b;
+  int64_t stride_s;
+  int64_t stride_h;
+} chorus_tensor;
+
+/* A CSR block mask (see conventions above).  All pointers are device pointers. */
+typedef struct {
+  int32_t mask_batch;       /* 1 or B                                           */
+  int32_t H;                /* heads; must equal the shape's H                  */
+  int32_t n_blocks;         /* ceil(S / block); q-blocks = kv-blocks per head   */
+  int32_t block;            /* tokens per block; must be 64                     */
+  const int32_t* row_ptr;   /* [mask_batch * H * n_blocks + 1], row_ptr[0] == 0 */
+  const int32_t* col_idx;   /* [nnz] ascending kv-block ids per row             */
+} chorus_block_mask;
+
+/* Optional work order for the attention kernels (see chorus_plan_block_mask). */
+typedef struct {
+  const int32_t* order;     /* [B * H * n_blocks] permutation of work items     */
+  int32_t n_items;          /* must equal B * H * n_blocks                       */
+} chorus_schedule;
+
+/* ---------------------------------------------------------------------------
+ * Mask builder -- Sec. 3.2 Obs. 2 (score = softmax(mean(Q) mean(K)^T)),
+ * Sec. 3.2 "Mask Caching and Retrieval" (top-p with a top-k floor), Sec. 3.2
+ * "Minimum top-k guarantee", Sec. 4.1 (top_p, min_top_k).
+ *
+ * For every request b in [0, B) and head h it computes, in order:
+ *   1. q_i, k_j: mean of Q / K over the valid tokens of block i / j
+ *      (float64 accumulation, divided by the valid-token count);
+ *   2. s_ij = sm_scale * <q_i, k_j> in float64;
+ *   3. p_ij = softmax over j of s_ij;
+ *   4. the order of j by (s_ij descending, j ascending);
+ *   5. k_p = smallest k >= 1 whose cumulative p in that order is >= top_p
+ *      (0 if top_p <= 0, n_blocks if top_p >= 1);
+ *   6. k_min = ceil(min_top_k * n_blocks - 1e-9);
+ *   7. keeps the first min(n_blocks, max(k_p, k_min, 1)) blocks of the order
+ *      and writes them ascending as CSR row (b * H + h) * n_blocks + i.
+ * The result has mask_batch = B.  To build one mask from one request (and
+ * reuse it for others), pass a B = 1 view of that request.
+ *
+ * q, k          : [B, S, H, D] f16 or bf16 (dtype), read only.
+ * row_ptr       : out, device int32 [B * H * n_blocks + 1].
+ * col_idx       : out, device int32 [col_capacity]; col_capacity must be at
+ *                 least B * H * n_blocks * n_blocks (the worst case, since the
+ *                 count is only known on device) else CHORUS_ERR_CAPACITY.
+ * block_scores  : optional out (NULL to skip), device float32
+ *                 [B * H * n_blocks, n_blocks]: s_ij rounded to fp32.
+ * workspace     : device scratch of at least
+ *                 chorus_build_block_mask_workspace_size(shape) bytes,
+ *                 256-byte aligned; contents on entry are ignored.
+ * Supports n_blocks <= 4096 (S <= 262144).
+ * ------------------------------------------------------------------------- */
+size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape);
+chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
+                                      const chorus_tensor* q, const chorus_tensor* k,
+                                      double sm_scale, double top_p, double min_top_k,
+                                      int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                      float* block_scores, void* workspace,
+                                      size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Work plan -- the one-GPU counterpart of the paper's head-level scheduling
+ * (Sec. 3.2 "Head-level scheduling for load balancing", Appendix A): because
+ * a reused mask's per-head cost is known before the attention runs, the work
+ * can be placed ahead of time.  Here the work items (b, h, i) of one attention
+ * call are split into 8 contiguous runs of near-equal cost (cost = listed
+ * blocks + 1), one per XCD, and written interleaved so that dispatch position
+ * p runs on XCD p mod 8; within an XCD items keep their (b, h, i) order so
+ * neighbouring q-blocks of one head share L2.  Computed on device, once per
+ * mask, and reusable for every call that applies the same mask to B requests.
+ *
+ * order         : out, device int32 [B * H * n_blocks] (a permutation).
+ * workspace     : device scratch of chorus_plan_workspace_size() bytes.
+ * The plan only changes performance, never results.
+ * ------------------------------------------------------------------------- */
+size_t chorus_plan_workspace_size(const chorus_shape* shape, const chorus_block_mask* mask);
+chorus_status chorus_plan_block_mask(const chorus_shape* shape, const chorus_block_mask* mask,
+                                     int32_t* order, void* workspace, size_t workspace_bytes,
+                                     void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Mask check for masks that come from outside the builder.  Writes into
+ * *d_flags (device int32, overwritten) the OR of: 1 = row_ptr[0] != 0,
+ * 2 = row_ptr decreasing, 4 = col_idx out of [0, n_blocks),
+ * 8 = col_idx not strictly ascending within a row, 16 = nnz > col_capacity.
+ * 0 means valid.  Stream-ordered; the caller reads the flag when it needs it.
+ * ------------------------------------------------------------------------- */
+chorus_status chorus_validate_block_mask(const chorus_block_mask* mask, int64_t col_capacity,
+                                         int32_t* d_flags, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * FP8 blockwise quantiser for the FP8 path (Sec. 3.2 "Efficient block-sparse
+ * kernel": FP8 matrix products with high-precision accumulation).  For every
+ * (b, h, 64-token block) over its valid tokens x 128 values:
+ *   amax = max|x|; inv = fp32(448 / amax); code = e4m3fn_rne(clamp(x * inv,
+ *   -448, 448)); scale = fp32(amax / 448); amax == 0 gives codes +-0, scale 1.
+ * x      : [B, S, H, D] f16 or bf16 (in_dtype).
+ * codes  : out [B, S, H, D] uint8 (its own strides, in bytes == elements).
+ * scales : out device float32 [B, H, n_blocks], contiguous.
+ * ------------------------------------------------------------------------- */
+chorus_status chorus_quantize_fp8_blockwise(chorus_dtype in_dtype, const chorus_shape* shape,
+                                            const chorus_tensor* x, const chorus_tensor* codes,
+                                            float* scales, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Block-sparse attention forward -- Sec. 3.2 "Efficient block-sparse kernel":
+ * for every request b, head h and query token r < S in q-block i, with mask
+ * row m = ((mask_batch > 1 ? b : 0) * H + h) * n_blocks + i,
+ *   O[b,r,h,:] = sum_{c in A} softmax_c(sm_scale <Q[b,r,h,:], K[b,c,h,:]>) V[b,c,h,:]
+ * over A = { c < S : c / 64 listed in row m }, and
+ *   lse[b,h,r] = ln sum_{c in A} exp(sm_scale <Q[b,r,h,:], K[b,c,h,:]>).
+ * An empty row gives O = 0 and lse = -inf.
+ *
+ * dtype = CHORUS_F16 / CHORUS_BF16: q, k, v, out in that type; scales NULL.
+ * dtype = CHORUS_FP8_E4M3: q, k, v are e4m3fn codes with fp32 block scales
+ *   q_scale, k_scale, v_scale [B, H, n_blocks] (as written by the quantiser);
+ *   the values read are code * scale.  QK^T and PV run as FP8 MFMA with fp32
+ *   accumulation; P is rounded to e4m3 for PV.  out is bf16.
+ * lse      : optional out (NULL to skip), device float32 [B, H, S] contiguous.
+ * schedule : optional work order from chorus_plan_block_mask (NULL = the
+ *            library's default order); never changes results.
+ * workspace: device scratch of chorus_attn_workspace_size() bytes (may be 0).
+ * Results are bitwise deterministic for a given input, mask and dtype.
+ * ------------------------------------------------------------------------- */
+size_t chorus_attn_workspace_size(chorus_dtype dtype, const chorus_shape* shape,
+                                  const chorus_block_mask* mask);
+chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shape* shape,
+                                           const chorus_tensor* q, const chorus_tensor* k,
+                                           const chorus_tensor* v, const float* q_scale,
+                                           const float* k_scale, const float* v_scale,
+                                           const chorus_block_mask* mask,
+                                           const chorus_schedule* schedule, float sm_scale,
+                                           const chorus_tensor* out, float* lse, void* workspace,
+                                           size_t workspace_bytes, void* stream);
+
+/* Typed conveniences for the generic entry point above (same semantics). */
+chorus_status chorus_block_sparse_attn_fwd_f16(const chorus_shape* shape, const chorus_tensor* q,
+                                               const chorus_tensor* k, const chorus_tensor* v,
+                                               const chorus_block_mask* mask,
+                                               const chorus_schedule* schedule, float sm_scale,
+                                               const chorus_tensor* out, float* lse,
+                                               void* workspace, size_t workspace_bytes,
+                                               void* stream);
+chorus_status chorus_block_sparse_attn_fwd_bf16(const chorus_shape* shape, const chorus_tensor* q,
+                                                const chorus_tensor* k, const chorus_tensor* v,
+                                                const chorus_block_mask* mask,
+                                                const chorus_schedule* schedule, float sm_scale,
+                                                const chorus_tensor* out, float* lse,
+                                                void* workspace, size_t workspace_bytes,
+                                                void* stream);
+chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const chorus_tensor* q,
+                                               const chorus_tensor* k, const chorus_tensor* v,
+                                               const float* q_scale, const float* k_scale,
+                                               const float* v_scale,
+                                               const chorus_block_mask* mask,
+                                               const chorus_schedule* schedule, float sm_scale,
+                                               const chorus_tensor* out, float* lse,
+                                               void* workspace, size_t workspace_bytes,
+                                               void* stream);
+
+/* Human-readable name of a status, and the detail of the calling thread's
+ * last error (empty string if none).  Both return static / thread-local
+ * storage owned by the library. */
+const char* chorus_status_string(chorus_status status);
+const char* chorus_last_error(void);
+
+/* Library version as MAJOR * 10000 + MINOR * 100 + PATCH. */
+int32_t chorus_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CHORUS_H_ */

@@ -1,0 +1,316 @@
+// Host side of the C ABI: argument validation, workspace carving, dispatch.
+// Nothing here allocates device memory or synchronises; all work is enqueued
+// on the caller's stream.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "chorus_internal.h"
+
+namespace chorus {
+
+static thread_local char g_last_error[512] = "";
+
+chorus_status fail(chorus_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+chorus_status check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(CHORUS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return CHORUS_OK;
+}
+
+static chorus_status from_hip(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(CHORUS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return check_launch(what);
+}
+
+static size_t elem_size(chorus_dtype dt) { return dt == CHORUS_FP8_E4M3 ? 1 : 2; }
+
+static chorus_status check_shape(const chorus_shape* s) {
+  if (!s) return fail(CHORUS_ERR_INVALID_ARG, "shape is NULL");
+  if (s->B < 1 || s->S < 1 || s->H < 1)
+    return fail(CHORUS_ERR_INVALID_ARG, "shape B=%d S=%d H=%d must be >= 1", s->B, s->S, s->H);
+  if (s->D != kHeadDim)
+    return fail(CHORUS_ERR_UNSUPPORTED, "head dim D=%d unsupported (only 128)", s->D);
+  return CHORUS_OK;
+}
+
+static chorus_status check_tensor(const chorus_tensor* t, const char* name, size_t esize) {
+  if (!t) return fail(CHORUS_ERR_INVALID_ARG, "%s descriptor is NULL", name);
+  if (!t->data) return fail(CHORUS_ERR_INVALID_ARG, "%s data pointer is NULL", name);
+  if (reinterpret_cast<uintptr_t>(t->data) % 16)
+    return fail(CHORUS_ERR_INVALID_ARG, "%s data pointer is not 16-byte aligned", name);
+  const int64_t st[3] = {t->stride_b, t->stride_s, t->stride_h};
+  for (int i = 0; i < 3; ++i) {
+    if (st[i] < 0) return fail(CHORUS_ERR_INVALID_ARG, "%s has a negative stride", name);
+    if ((st[i] * (int64_t)esize) % 16)
+      return fail(CHORUS_ERR_INVALID_ARG, "%s stride %lld elements breaks 16-byte row alignment",
+                  name, (long long)st[i]);
+  }
+  return CHORUS_OK;
+}
+
+static TensorArg targ(const chorus_tensor* t) { return {t->data, t->stride_b, t->stride_s, t->stride_h}; }
+
+static chorus_status check_mask(const chorus_shape* s, const chorus_block_mask* m) {
+  if (!m) return fail(CHORUS_ERR_INVALID_ARG, "mask is NULL");
+  if (m->block != kBlock) return fail(CHORUS_ERR_UNSUPPORTED, "mask block %d unsupported (only 64)", m->block);
+  if (m->mask_batch != 1 && m->mask_batch != s->B)
+    return fail(CHORUS_ERR_INVALID_ARG, "mask_batch %d must be 1 or B=%d", m->mask_batch, s->B);
+  if (m->H != s->H) return fail(CHORUS_ERR_INVALID_ARG, "mask H=%d != shape H=%d", m->H, s->H);
+  if (m->n_blocks != blocks_of(s->S))
+    return fail(CHORUS_ERR_INVALID_ARG, "mask n_blocks=%d != ceil(S/64)=%d", m->n_blocks, blocks_of(s->S));
+  if (!m->row_ptr || !m->col_idx) return fail(CHORUS_ERR_INVALID_ARG, "mask row_ptr/col_idx is NULL");
+  return CHORUS_OK;
+}
+
+static chorus_status check_workspace(void* ws, size_t have, size_t need) {
+  if (need == 0) return CHORUS_OK;
+  if (!ws) return fail(CHORUS_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(CHORUS_ERR_WORKSPACE, "workspace not 256-byte aligned");
+  if (have < need) return fail(CHORUS_ERR_WORKSPACE, "workspace %zu bytes < required %zu", have, need);
+  return CHORUS_OK;
+}
+
+BuilderWorkspace carve_builder(void* ws, int B, int H, int n, size_t* bytes) {
+  Carver c(ws);
+  BuilderWorkspace w;
+  const size_t rows = (size_t)B * H * n;
+  w.words = (n + 31) / 32;
+  w.qbar = c.take<double>(rows * kHeadDim);
+  w.kbar = c.take<double>(rows * kHeadDim);
+  w.counts = c.take<int32_t>(rows);
+  w.bitmap = c.take<uint32_t>(rows * w.words);
+  w.scores = c.take<double>(rows * n);
+  if (bytes) *bytes = align_up(c.used, 256);
+  return w;
+}
+
+}  // namespace chorus
+
+using namespace chorus;
+
+extern "C" {
+
+const char* chorus_status_string(chorus_status s) {
+  switch (s) {
+    case CHORUS_OK: return "CHORUS_OK";
+    case CHORUS_ERR_INVALID_ARG: return "CHORUS_ERR_INVALID_ARG";
+    case CHORUS_ERR_UNSUPPORTED: return "CHORUS_ERR_UNSUPPORTED";
+    case CHORUS_ERR_CAPACITY: return "CHORUS_ERR_CAPACITY";
+    case CHORUS_ERR_HIP: return "CHORUS_ERR_HIP";
+    case CHORUS_ERR_WORKSPACE: return "CHORUS_ERR_WORKSPACE";
+  }
+  return "CHORUS_ERR_UNKNOWN";
+}
+
+const char* chorus_last_error(void) { return g_last_error; }
+
+int32_t chorus_version(void) { return 100; }
+
+size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape) {
+  if (!shape || shape->B < 1 || shape->S < 1 || shape->H < 1) return 0;
+  size_t bytes = 0;
+  carve_builder(nullptr, shape->B, shape->H, blocks_of(shape->S), &bytes);
+  return bytes;
+}
+
+chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
+                                      const chorus_tensor* q, const chorus_tensor* k,
+                                      double sm_scale, double top_p, double min_top_k,
+                                      int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                      float* block_scores, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if (dtype != CHORUS_F16 && dtype != CHORUS_BF16)
+    return fail(CHORUS_ERR_UNSUPPORTED, "builder input dtype %d unsupported (f16/bf16)", (int)dtype);
+  if ((st = check_tensor(q, "q", 2))) return st;
+  if ((st = check_tensor(k, "k", 2))) return st;
+  const int n = blocks_of(shape->S);
+  if (n > kMaxBuilderBlocks)
+    return fail(CHORUS_ERR_UNSUPPORTED, "n_blocks=%d exceeds builder limit %d", n, kMaxBuilderBlocks);
+  if (!(top_p >= 0.0 && top_p <= 1.0)) return fail(CHORUS_ERR_INVALID_ARG, "top_p must be in [0, 1]");
+  if (!(min_top_k >= 0.0 && min_top_k <= 1.0))
+    return fail(CHORUS_ERR_INVALID_ARG, "min_top_k must be in [0, 1]");
+  if (!std::isfinite(sm_scale)) return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite");
+  if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
+  const int64_t rows = (int64_t)shape->B * shape->H * n;
+  if (rows * n > INT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "B*H*n_blocks^2 = %lld exceeds int32 CSR offsets", (long long)(rows * n));
+  if (col_capacity < rows * n)
+    return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
+                (long long)(rows * n));
+  size_t need = 0;
+  BuilderWorkspace w = carve_builder(workspace, shape->B, shape->H, n, &need);
+  if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
+  const int k_min = (int)std::ceil(min_top_k * (double)n - 1e-9);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = from_hip(launch_pool(dtype, targ(q), targ(k), shape->B, shape->S, shape->H, w.qbar, w.kbar, s),
+                     "pool")))
+    return st;
+  if ((st = from_hip(launch_score_select(w.qbar, w.kbar, shape->B, shape->H, n, sm_scale, top_p,
+                                         k_min, w.scores, w.counts, w.bitmap, w.words, block_scores, s),
+                     "score_select")))
+    return st;
+  if ((st = from_hip(launch_scan_counts(w.counts, rows, row_ptr, s), "scan"))) return st;
+  return from_hip(launch_compact(w.bitmap, w.words, row_ptr, rows, col_idx, s), "compact");
+}
+
+size_t chorus_plan_workspace_size(const chorus_shape* shape, const chorus_block_mask* mask) {
+  (void)mask;
+  if (!shape || shape->B < 1 || shape->H < 1) return 0;
+  return align_up((size_t)shape->B * shape->H * sizeof(int32_t), 256);
+}
+
+chorus_status chorus_plan_block_mask(const chorus_shape* shape, const chorus_block_mask* mask,
+                                     int32_t* order, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if ((st = check_mask(shape, mask))) return st;
+  if (!order) return fail(CHORUS_ERR_INVALID_ARG, "order is NULL");
+  if ((st = check_workspace(workspace, workspace_bytes, chorus_plan_workspace_size(shape, mask)))) return st;
+  return from_hip(launch_plan(mask->row_ptr, mask->mask_batch, shape->B, shape->H, mask->n_blocks,
+                              static_cast<int32_t*>(workspace), order, static_cast<hipStream_t>(stream)),
+                  "plan");
+}
+
+chorus_status chorus_validate_block_mask(const chorus_block_mask* mask, int64_t col_capacity,
+                                         int32_t* d_flags, void* stream) {
+  g_last_error[0] = 0;
+  if (!mask || !mask->row_ptr || !mask->col_idx || !d_flags)
+    return fail(CHORUS_ERR_INVALID_ARG, "mask, its arrays and d_flags must be non-NULL");
+  if (mask->mask_batch < 1 || mask->H < 1 || mask->n_blocks < 1)
+    return fail(CHORUS_ERR_INVALID_ARG, "mask dimensions must be >= 1");
+  const int64_t rows = (int64_t)mask->mask_batch * mask->H * mask->n_blocks;
+  return from_hip(launch_validate(mask->row_ptr, mask->col_idx, rows, mask->n_blocks, col_capacity, d_flags,
+                                  static_cast<hipStream_t>(stream)),
+                  "validate");
+}
+
+chorus_status chorus_quantize_fp8_blockwise(chorus_dtype in_dtype, const chorus_shape* shape,
+                                            const chorus_tensor* x, const chorus_tensor* codes,
+                                            float* scales, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if (in_dtype != CHORUS_F16 && in_dtype != CHORUS_BF16)
+    return fail(CHORUS_ERR_UNSUPPORTED, "quantiser input dtype %d unsupported (f16/bf16)", (int)in_dtype);
+  if ((st = check_tensor(x, "x", 2))) return st;
+  if ((st = check_tensor(codes, "codes", 1))) return st;
+  if (!scales) return fail(CHORUS_ERR_INVALID_ARG, "scales is NULL");
+  return from_hip(launch_quant_fp8(in_dtype, targ(x), targ(codes), shape->B, shape->S, shape->H, scales,
+                                   static_cast<hipStream_t>(stream)),
+                  "quant_fp8");
+}
+
+size_t chorus_attn_workspace_size(chorus_dtype dtype, const chorus_shape* shape, const chorus_block_mask* mask) {
+  (void)dtype;
+  (void)shape;
+  (void)mask;
+  return 0;
+}
+
+chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shape* shape,
+                                           const chorus_tensor* q, const chorus_tensor* k,
+                                           const chorus_tensor* v, const float* q_scale,
+                                           const float* k_scale, const float* v_scale,
+                                           const chorus_block_mask* mask,
+                                           const chorus_schedule* schedule, float sm_scale,
+                                           const chorus_tensor* out, float* lse, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if (dtype != CHORUS_F16 && dtype != CHORUS_BF16 && dtype != CHORUS_FP8_E4M3)
+    return fail(CHORUS_ERR_UNSUPPORTED, "attention dtype %d unsupported", (int)dtype);
+  const size_t es = elem_size(dtype);
+  if ((st = check_tensor(q, "q", es))) return st;
+  if ((st = check_tensor(k, "k", es))) return st;
+  if ((st = check_tensor(v, "v", es))) return st;
+  if ((st = check_tensor(out, "out", 2))) return st;
+  if ((st = check_mask(shape, mask))) return st;
+  if (dtype == CHORUS_FP8_E4M3) {
+    if (!q_scale || !k_scale || !v_scale)
+      return fail(CHORUS_ERR_INVALID_ARG, "fp8 attention needs q_scale, k_scale and v_scale");
+  } else if (q_scale || k_scale || v_scale) {
+    return fail(CHORUS_ERR_INVALID_ARG, "scales are only accepted for fp8 attention");
+  }
+  if (!std::isfinite(sm_scale) || !(sm_scale > 0.f))
+    return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite and > 0");
+  const int n = mask->n_blocks;
+  const int64_t items = (int64_t)shape->B * shape->H * n;
+  if (items > INT32_MAX) return fail(CHORUS_ERR_UNSUPPORTED, "too many work items");
+  if (schedule) {
+    if (!schedule->order) return fail(CHORUS_ERR_INVALID_ARG, "schedule order is NULL");
+    if (schedule->n_items != items)
+      return fail(CHORUS_ERR_INVALID_ARG, "schedule has %d items, expected %lld", schedule->n_items,
+                  (long long)items);
+  }
+  if ((st = check_workspace(workspace, workspace_bytes, chorus_attn_workspace_size(dtype, shape, mask))))
+    return st;
+  AttnArgs a;
+  a.q = targ(q);
+  a.k = targ(k);
+  a.v = targ(v);
+  a.o = targ(out);
+  a.q_scale = q_scale;
+  a.k_scale = k_scale;
+  a.v_scale = v_scale;
+  a.row_ptr = mask->row_ptr;
+  a.col_idx = mask->col_idx;
+  a.order = schedule ? schedule->order : nullptr;
+  a.lse = lse;
+  a.B = shape->B;
+  a.S = shape->S;
+  a.H = shape->H;
+  a.n = n;
+  a.mask_batch = mask->mask_batch;
+  a.sm_scale = sm_scale;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == CHORUS_FP8_E4M3) return from_hip(launch_attn_fwd_fp8(a, s), "attn_fwd_fp8");
+  return from_hip(launch_attn_fwd_16(dtype, a, s), "attn_fwd");
+}
+
+chorus_status chorus_block_sparse_attn_fwd_f16(const chorus_shape* shape, const chorus_tensor* q,
+                                               const chorus_tensor* k, const chorus_tensor* v,
+                                               const chorus_block_mask* mask,
+                                               const chorus_schedule* schedule, float sm_scale,
+                                               const chorus_tensor* out, float* lse, void* workspace,
+                                               size_t workspace_bytes, void* stream) {
+  return chorus_block_sparse_attn_fwd(CHORUS_F16, shape, q, k, v, nullptr, nullptr, nullptr, mask, schedule,
+                                      sm_scale, out, lse, workspace, workspace_bytes, stream);
+}
+
+chorus_status chorus_block_sparse_attn_fwd_bf16(const chorus_shape* shape, const chorus_tensor* q,
+                                                const chorus_tensor* k, const chorus_tensor* v,
+                                                const chorus_block_mask* mask,
+                                                const chorus_schedule* schedule, float sm_scale,
+                                                const chorus_tensor* out, float* lse, void* workspace,
+                                                size_t workspace_bytes, void* stream) {
+  return chorus_block_sparse_attn_fwd(CHORUS_BF16, shape, q, k, v, nullptr, nullptr, nullptr, mask, schedule,
+                                      sm_scale, out, lse, workspace, workspace_bytes, stream);
+}
+
+chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const chorus_tensor* q,
+                                               const chorus_tensor* k, const chorus_tensor* v,
+                                               const float* q_scale, const float* k_scale,
+                                               const float* v_scale, const chorus_block_mask* mask,
+                                               const chorus_schedule* schedule, float sm_scale,
+                                               const chorus_tensor* out, float* lse, void* workspace,
+                                               size_t workspace_bytes, void* stream) {
+  return chorus_block_sparse_attn_fwd(CHORUS_FP8_E4M3, shape, q, k, v, q_scale, k_scale, v_scale, mask,
+                                      schedule, sm_scale, out, lse, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"

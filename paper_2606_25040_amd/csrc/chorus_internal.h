@@ -1,0 +1,90 @@
+// Internal declarations shared by the host API and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "chorus.h"
+
+namespace chorus {
+
+constexpr int kBlock = 64;            // tokens per mask block
+constexpr int kHeadDim = 128;         // supported head dim
+constexpr int kMaxBuilderBlocks = 4096;
+constexpr int kNumXcd = 8;            // MI355X: 8 XCDs x 32 CUs
+
+// Record a formatted error for chorus_last_error(); returns `st` for chaining.
+chorus_status fail(chorus_status st, const char* fmt, ...);
+chorus_status check_launch(const char* what);
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+inline int32_t blocks_of(int32_t S) { return (S + kBlock - 1) / kBlock; }
+
+// Carves a workspace into 256-byte aligned segments.
+struct Carver {
+  char* base;
+  size_t used = 0;
+  explicit Carver(void* p) : base(static_cast<char*>(p)) {}
+  template <class T>
+  T* take(size_t count) {
+    used = align_up(used, 256);
+    T* p = base ? reinterpret_cast<T*>(base + used) : nullptr;
+    used += count * sizeof(T);
+    return p;
+  }
+};
+
+// Plain-old-data view of one [B, S, H, D] tensor for kernels.
+struct TensorArg {
+  const void* data;
+  int64_t sb, ss, sh;
+};
+
+// ---- mask builder (mask_builder.hip) ----
+struct BuilderWorkspace {
+  double* qbar;      // [B*H*n, D]
+  double* kbar;      // [B*H*n, D]
+  int32_t* counts;   // [B*H*n]
+  uint32_t* bitmap;  // [B*H*n, words]
+  double* scores;    // [B*H*n, n]
+  int32_t words;
+};
+BuilderWorkspace carve_builder(void* ws, int B, int H, int n, size_t* bytes);
+hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, double* qbar,
+                       double* kbar, hipStream_t st);
+hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n,
+                               double sm_scale, double top_p, int k_min, double* scores,
+                               int32_t* counts, uint32_t* bitmap, int words, float* block_scores,
+                               hipStream_t st);
+hipError_t launch_scan_counts(const int32_t* counts, int64_t rows, int32_t* row_ptr, hipStream_t st);
+hipError_t launch_compact(const uint32_t* bitmap, int words, const int32_t* row_ptr, int64_t rows,
+                          int32_t* col_idx, hipStream_t st);
+hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n,
+                       int32_t* unit_cost_ws, int32_t* order, hipStream_t st);
+hipError_t launch_validate(const int32_t* row_ptr, const int32_t* col_idx, int64_t rows, int n,
+                           int64_t capacity, int32_t* flags, hipStream_t st);
+
+// ---- fp8 quantiser (quant_fp8.hip) ----
+hipError_t launch_quant_fp8(chorus_dtype in_dt, TensorArg x, TensorArg codes, int B, int S, int H,
+                            float* scales, hipStream_t st);
+
+// ---- attention (attn_fwd.hip, attn_fwd_fp8.hip) ----
+struct AttnArgs {
+  TensorArg q, k, v, o;
+  const float* q_scale;
+  const float* k_scale;
+  const float* v_scale;
+  const int32_t* row_ptr;
+  const int32_t* col_idx;
+  const int32_t* order;   // nullable
+  float* lse;             // nullable
+  int B, S, H, n;
+  int mask_batch;
+  float sm_scale;
+};
+hipError_t launch_attn_fwd_16(chorus_dtype dt, const AttnArgs& a, hipStream_t st);
+hipError_t launch_attn_fwd_fp8(const AttnArgs& a, hipStream_t st);
+
+}  // namespace chorus

@@ -1,0 +1,318 @@
+"""Thin ctypes binding of libchorus.so (C ABI in include/chorus.h).
+
+Argument marshalling only: torch tensors are used for device memory and the
+current HIP stream; every step of the mask builder, the plan, the FP8
+quantiser and the attention runs in the library's HIP kernels.  There is no
+fallback: if the library is missing or a call fails, a RuntimeError is raised.
+
+Function names follow the C entry points without their ``chorus_`` prefix.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libchorus.so")
+
+F16, BF16, FP8_E4M3 = 0, 1, 2
+BLOCK = 64
+_STATUS = {0: "CHORUS_OK", 1: "CHORUS_ERR_INVALID_ARG", 2: "CHORUS_ERR_UNSUPPORTED",
+           3: "CHORUS_ERR_CAPACITY", 4: "CHORUS_ERR_HIP", 5: "CHORUS_ERR_WORKSPACE"}
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("S", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("D", ctypes.c_int32)]
+
+
+class Tensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("stride_b", ctypes.c_int64),
+                ("stride_s", ctypes.c_int64), ("stride_h", ctypes.c_int64)]
+
+
+class Mask(ctypes.Structure):
+    _fields_ = [("mask_batch", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("n_blocks", ctypes.c_int32), ("block", ctypes.c_int32),
+                ("row_ptr", ctypes.c_void_p), ("col_idx", ctypes.c_void_p)]
+
+
+class Schedule(ctypes.Structure):
+    _fields_ = [("order", ctypes.c_void_p), ("n_items", ctypes.c_int32)]
+
+
+EXPORTS = [
+    "chorus_build_block_mask_workspace_size", "chorus_build_block_mask",
+    "chorus_plan_workspace_size", "chorus_plan_block_mask", "chorus_validate_block_mask",
+    "chorus_quantize_fp8_blockwise", "chorus_attn_workspace_size",
+    "chorus_block_sparse_attn_fwd", "chorus_block_sparse_attn_fwd_f16",
+    "chorus_block_sparse_attn_fwd_bf16", "chorus_block_sparse_attn_fwd_fp8",
+    "chorus_status_string", "chorus_last_error", "chorus_version",
+]
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libchorus.so (once) and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -m paper_2606_25040_amd.build` "
+                           "(or __graft_entry__.build())")
+    L = ctypes.CDLL(path)
+    P, VP, I32, I64, F32, F64, SZ = (ctypes.POINTER, ctypes.c_void_p, ctypes.c_int32,
+                                    ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_size_t)
+    sig = {
+        "chorus_build_block_mask_workspace_size": (SZ, [P(Shape)]),
+        "chorus_build_block_mask": (I32, [I32, P(Shape), P(Tensor), P(Tensor), F64, F64, F64, VP, VP,
+                                          I64, VP, VP, SZ, VP]),
+        "chorus_plan_workspace_size": (SZ, [P(Shape), P(Mask)]),
+        "chorus_plan_block_mask": (I32, [P(Shape), P(Mask), VP, VP, SZ, VP]),
+        "chorus_validate_block_mask": (I32, [P(Mask), I64, VP, VP]),
+        "chorus_quantize_fp8_blockwise": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, VP]),
+        "chorus_attn_workspace_size": (SZ, [I32, P(Shape), P(Mask)]),
+        "chorus_block_sparse_attn_fwd": (I32, [I32, P(Shape), P(Tensor), P(Tensor), P(Tensor), VP,
+                                               VP, VP, P(Mask), P(Schedule), F32, P(Tensor), VP,
+                                               VP, SZ, VP]),
+        "chorus_block_sparse_attn_fwd_f16": (I32, [P(Shape), P(Tensor), P(Tensor), P(Tensor),
+                                                   P(Mask), P(Schedule), F32, P(Tensor), VP, VP,
+                                                   SZ, VP]),
+        "chorus_block_sparse_attn_fwd_bf16": (I32, [P(Shape), P(Tensor), P(Tensor), P(Tensor),
+                                                    P(Mask), P(Schedule), F32, P(Tensor), VP, VP,
+                                                    SZ, VP]),
+        "chorus_block_sparse_attn_fwd_fp8": (I32, [P(Shape), P(Tensor), P(Tensor), P(Tensor), VP,
+                                                   VP, VP, P(Mask), P(Schedule), F32, P(Tensor),
+                                                   VP, VP, SZ, VP]),
+        "chorus_status_string": (ctypes.c_char_p, [I32]),
+        "chorus_last_error": (ctypes.c_char_p, []),
+        "chorus_version": (I32, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(status: int, what: str) -> None:
+    if status != 0:
+        L = load_library()
+        raise RuntimeError(f"{what} failed: {_STATUS.get(status, status)}: "
+                           f"{L.chorus_last_error().decode()}")
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float16:
+        return F16
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.uint8:
+        return FP8_E4M3
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _tensor(t: torch.Tensor) -> Tensor:
+    if t.dim() != 4:
+        raise ValueError("expected a [B, S, H, D] tensor")
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if t.stride(3) != 1:
+        raise ValueError("head dim must be contiguous")
+    return Tensor(t.data_ptr(), t.stride(0), t.stride(1), t.stride(2))
+
+
+def _shape(t: torch.Tensor) -> Shape:
+    B, S, H, D = t.shape
+    return Shape(B, S, H, D)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor | None:
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+
+
+def _aligned(ws: torch.Tensor | None) -> int | None:
+    if ws is None:
+        return None
+    p = ws.data_ptr()
+    return (p + 255) // 256 * 256
+
+
+@dataclass
+class BlockMask:
+    """CSR block mask on device (rows (b_m * H + h) * n_blocks + i, ascending ids)."""
+    row_ptr: torch.Tensor      # int32 [mask_batch * H * n_blocks + 1]
+    col_idx: torch.Tensor      # int32 [capacity]
+    mask_batch: int
+    H: int
+    n_blocks: int
+    block: int = BLOCK
+    block_scores: torch.Tensor | None = None
+
+    @property
+    def rows(self) -> int:
+        return self.mask_batch * self.H * self.n_blocks
+
+    @property
+    def nnz(self) -> int:
+        return int(self.row_ptr[-1].item())
+
+    @property
+    def density(self) -> float:
+        return self.nnz / float(self.rows * self.n_blocks)
+
+    def as_c(self) -> Mask:
+        return Mask(self.mask_batch, self.H, self.n_blocks, self.block, self.row_ptr.data_ptr(),
+                    self.col_idx.data_ptr())
+
+    def to_host(self):
+        """(row_ptr, col_idx[:nnz]) as int64 numpy arrays."""
+        rp = self.row_ptr.cpu().numpy().astype("int64")
+        return rp, self.col_idx[: int(rp[-1])].cpu().numpy().astype("int64")
+
+    @staticmethod
+    def from_host(row_ptr, col_idx, mask_batch: int, H: int, n_blocks: int, device="cuda"):
+        rp = torch.as_tensor(row_ptr, dtype=torch.int32).to(device)
+        ci = torch.as_tensor(col_idx, dtype=torch.int32)
+        if ci.numel() == 0:
+            ci = torch.zeros(1, dtype=torch.int32)
+        return BlockMask(rp, ci.to(device), mask_batch, H, n_blocks)
+
+
+def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: float,
+                     sm_scale: float | None = None, return_scores: bool = False,
+                     out: BlockMask | None = None, workspace: torch.Tensor | None = None) -> BlockMask:
+    """chorus_build_block_mask: one mask per request of ``q, k [B, S, H, D]``."""
+    L = load_library()
+    if q.shape != k.shape or q.dtype != k.dtype:
+        raise ValueError("q and k must share shape and dtype")
+    B, S, H, D = q.shape
+    n = (S + BLOCK - 1) // BLOCK
+    rows = B * H * n
+    shape = _shape(q)
+    sm = 1.0 / math.sqrt(D) if sm_scale is None else float(sm_scale)
+    if out is None:
+        out = BlockMask(torch.empty(rows + 1, dtype=torch.int32, device=q.device),
+                        torch.empty(rows * n, dtype=torch.int32, device=q.device), B, H, n)
+    if return_scores and out.block_scores is None:
+        out.block_scores = torch.empty((rows, n), dtype=torch.float32, device=q.device)
+    need = L.chorus_build_block_mask_workspace_size(ctypes.byref(shape))
+    if workspace is None or workspace.numel() < need + 256:
+        workspace = _workspace(need, q.device)
+    st = L.chorus_build_block_mask(
+        _dtype_code(q), ctypes.byref(shape), ctypes.byref(_tensor(q)), ctypes.byref(_tensor(k)),
+        sm, float(top_p), float(min_top_k), out.row_ptr.data_ptr(), out.col_idx.data_ptr(),
+        out.col_idx.numel(), _ptr(out.block_scores if return_scores else None),
+        _aligned(workspace), need, _stream())
+    _check(st, "chorus_build_block_mask")
+    return out
+
+
+def plan_block_mask(mask: BlockMask, B: int, S: int) -> torch.Tensor:
+    """chorus_plan_block_mask: work order for applying ``mask`` to B requests."""
+    L = load_library()
+    shape = Shape(B, S, mask.H, 128)
+    cm = mask.as_c()
+    order = torch.empty(B * mask.H * mask.n_blocks, dtype=torch.int32, device=mask.row_ptr.device)
+    need = L.chorus_plan_workspace_size(ctypes.byref(shape), ctypes.byref(cm))
+    ws = _workspace(need, mask.row_ptr.device)
+    st = L.chorus_plan_block_mask(ctypes.byref(shape), ctypes.byref(cm), order.data_ptr(),
+                                  _aligned(ws), need, _stream())
+    _check(st, "chorus_plan_block_mask")
+    return order
+
+
+def validate_block_mask(mask: BlockMask) -> int:
+    """chorus_validate_block_mask; synchronises and returns the flag word (0 = valid)."""
+    L = load_library()
+    flags = torch.empty(1, dtype=torch.int32, device=mask.row_ptr.device)
+    cm = mask.as_c()
+    st = L.chorus_validate_block_mask(ctypes.byref(cm), mask.col_idx.numel(), flags.data_ptr(),
+                                      _stream())
+    _check(st, "chorus_validate_block_mask")
+    return int(flags.item())
+
+
+def quantize_fp8_blockwise(x: torch.Tensor, codes: torch.Tensor | None = None,
+                           scales: torch.Tensor | None = None):
+    """chorus_quantize_fp8_blockwise: returns (codes uint8 [B,S,H,D], scales fp32 [B,H,n])."""
+    L = load_library()
+    B, S, H, D = x.shape
+    n = (S + BLOCK - 1) // BLOCK
+    if codes is None:
+        codes = torch.empty((B, S, H, D), dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty((B, H, n), dtype=torch.float32, device=x.device)
+    st = L.chorus_quantize_fp8_blockwise(_dtype_code(x), ctypes.byref(_shape(x)),
+                                         ctypes.byref(_tensor(x)), ctypes.byref(_tensor(codes)),
+                                         scales.data_ptr(), _stream())
+    _check(st, "chorus_quantize_fp8_blockwise")
+    return codes, scales
+
+
+def block_sparse_attn_fwd(q, k, v, mask: BlockMask, sm_scale: float | None = None,
+                          scales=None, out: torch.Tensor | None = None, return_lse: bool = False,
+                          schedule: torch.Tensor | None = None):
+    """chorus_block_sparse_attn_fwd (dtype taken from q: f16, bf16 or uint8 fp8 codes).
+
+    ``scales`` = (q_scale, k_scale, v_scale) for fp8 codes.  Returns ``out``
+    (and ``lse [B, H, S]`` fp32 when ``return_lse``).
+    """
+    L = load_library()
+    dt = _dtype_code(q)
+    B, S, H, D = q.shape
+    sm = 1.0 / math.sqrt(D) if sm_scale is None else float(sm_scale)
+    if out is None:
+        odt = torch.bfloat16 if dt == FP8_E4M3 else q.dtype
+        out = torch.empty((B, S, H, D), dtype=odt, device=q.device)
+    lse = torch.empty((B, H, S), dtype=torch.float32, device=q.device) if return_lse else None
+    qs = ks = vs = None
+    if dt == FP8_E4M3:
+        if scales is None:
+            raise ValueError("fp8 attention needs (q_scale, k_scale, v_scale)")
+        qs, ks, vs = (s.data_ptr() for s in scales)
+    shape = _shape(q)
+    cm = mask.as_c()
+    sched = None
+    if schedule is not None:
+        sched = ctypes.byref(Schedule(schedule.data_ptr(), schedule.numel()))
+    need = L.chorus_attn_workspace_size(dt, ctypes.byref(shape), ctypes.byref(cm))
+    ws = _workspace(need, q.device)
+    st = L.chorus_block_sparse_attn_fwd(dt, ctypes.byref(shape), ctypes.byref(_tensor(q)),
+                                        ctypes.byref(_tensor(k)), ctypes.byref(_tensor(v)), qs, ks,
+                                        vs, ctypes.byref(cm), sched, sm, ctypes.byref(_tensor(out)),
+                                        _ptr(lse), _aligned(ws), need, _stream())
+    _check(st, "chorus_block_sparse_attn_fwd")
+    return (out, lse) if return_lse else out
+
+
+def block_sparse_attn_fwd_f16(q, k, v, mask, **kw):
+    assert q.dtype == torch.float16
+    return block_sparse_attn_fwd(q, k, v, mask, **kw)
+
+
+def block_sparse_attn_fwd_bf16(q, k, v, mask, **kw):
+    assert q.dtype == torch.bfloat16
+    return block_sparse_attn_fwd(q, k, v, mask, **kw)
+
+
+def block_sparse_attn_fwd_fp8(q, k, v, q_scale, k_scale, v_scale, mask, **kw):
+    assert q.dtype == torch.uint8
+    return block_sparse_attn_fwd(q, k, v, mask, scales=(q_scale, k_scale, v_scale), **kw)

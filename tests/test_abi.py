@@ -1,0 +1,115 @@
+"""C ABI: the library loads, exports every declared symbol, and rejects bad
+arguments on the host before touching the GPU (CPU only: no kernel runs)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_25040_amd import ops
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "chorus.h")
+
+FAKE = 0x10000           # aligned, never dereferenced: every call below fails validation first
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ops.LIB_PATH):
+        pytest.fail("libchorus.so is not built (run __graft_entry__.build())")
+    return ops.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(chorus_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 14
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(ops.EXPORTS) == names
+
+
+def test_status_strings_and_version(lib):
+    assert lib.chorus_status_string(0) == b"CHORUS_OK"
+    assert lib.chorus_status_string(3) == b"CHORUS_ERR_CAPACITY"
+    assert lib.chorus_version() >= 100
+
+
+def t4(B=1, S=100, H=2):
+    return ops.Tensor(FAKE, S * H * 128, H * 128, 128)
+
+
+def shape(B=1, S=100, H=2, D=128):
+    return ops.Shape(B, S, H, D)
+
+
+def build(lib, shp, q=None, top_p=0.5, mk=0.1, cap=None, ws_bytes=None, dtype=ops.BF16):
+    n = (shp.S + 63) // 64
+    rows = shp.B * shp.H * n
+    cap = rows * n if cap is None else cap
+    need = lib.chorus_build_block_mask_workspace_size(ctypes.byref(shp))
+    ws = need if ws_bytes is None else ws_bytes
+    qq = q or t4(shp.B, shp.S, shp.H)
+    return lib.chorus_build_block_mask(dtype, ctypes.byref(shp), ctypes.byref(qq), ctypes.byref(qq),
+                                       0.088, top_p, mk, FAKE, FAKE, cap, None, FAKE, ws, None)
+
+
+def test_builder_argument_checks(lib):
+    assert build(lib, shape(D=64)) == 2
+    assert build(lib, shape(S=0)) == 1
+    assert build(lib, shape(), top_p=1.5) == 1
+    assert build(lib, shape(), top_p=float("nan")) == 1
+    assert build(lib, shape(), mk=-0.1) == 1
+    assert build(lib, shape(), cap=3) == 3
+    assert build(lib, shape(), ws_bytes=16) == 5
+    assert build(lib, shape(), dtype=ops.FP8_E4M3) == 2
+    assert build(lib, shape(S=64 * 4097)) == 2
+    bad = ops.Tensor(FAKE + 8, 100 * 2 * 128, 2 * 128, 128)
+    assert build(lib, shape(), q=bad) == 1
+    bad = ops.Tensor(FAKE, 100 * 2 * 128, 2 * 128 + 4, 128)
+    assert build(lib, shape(), q=bad) == 1
+    assert b"stride" in lib.chorus_last_error()
+
+
+def attn(lib, shp, mask, dtype=ops.BF16, scales=(None, None, None), sched=None, sm=0.088):
+    t = t4(shp.B, shp.S, shp.H)
+    return lib.chorus_block_sparse_attn_fwd(dtype, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
+                                            ctypes.byref(t), *scales, ctypes.byref(mask),
+                                            sched, sm, ctypes.byref(t), None, None, 0, None)
+
+
+def test_attention_argument_checks(lib):
+    shp = shape(B=2, S=100, H=2)
+    ok = ops.Mask(1, 2, 2, 64, FAKE, FAKE)
+    assert attn(lib, shp, ops.Mask(1, 2, 2, 128, FAKE, FAKE)) == 2     # block 128
+    assert attn(lib, shp, ops.Mask(3, 2, 2, 64, FAKE, FAKE)) == 1      # mask_batch
+    assert attn(lib, shp, ops.Mask(1, 3, 2, 64, FAKE, FAKE)) == 1      # H
+    assert attn(lib, shp, ops.Mask(1, 2, 3, 64, FAKE, FAKE)) == 1      # n_blocks
+    assert attn(lib, shp, ops.Mask(1, 2, 2, 64, None, FAKE)) == 1      # null row_ptr
+    assert attn(lib, shp, ok, dtype=ops.FP8_E4M3) == 1                 # fp8 without scales
+    assert attn(lib, shp, ok, scales=(FAKE, FAKE, FAKE)) == 1          # scales on bf16
+    assert attn(lib, shp, ok, dtype=7) == 2
+    assert attn(lib, shp, ok, sm=0.0) == 1
+    sched = ops.Schedule(FAKE, 5)
+    assert attn(lib, shp, ok, sched=ctypes.byref(sched)) == 1
+    assert attn(lib, shape(D=64), ok) == 2
+
+
+def test_other_entry_points_check_arguments(lib):
+    shp = shape()
+    t = t4()
+    assert lib.chorus_quantize_fp8_blockwise(ops.FP8_E4M3, ctypes.byref(shp), ctypes.byref(t),
+                                             ctypes.byref(t), FAKE, None) == 2
+    assert lib.chorus_quantize_fp8_blockwise(ops.BF16, ctypes.byref(shp), ctypes.byref(t),
+                                             ctypes.byref(t), None, None) == 1
+    m = ops.Mask(1, 2, 2, 64, FAKE, FAKE)
+    assert lib.chorus_plan_block_mask(ctypes.byref(shp), ctypes.byref(m), None, None, 0, None) == 1
+    assert lib.chorus_validate_block_mask(ctypes.byref(m), 10, None, None) == 1
+    assert lib.chorus_build_block_mask_workspace_size(ctypes.byref(shape(S=75600, H=40))) > 0

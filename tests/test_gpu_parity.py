@@ -1,0 +1,354 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Small cases compare every output; the full-size workloads compare sampled
+rows and work items the oracle computes one by one.  Tolerances: masks
+bit-exact apart from excused near-ties (tests/compare.py); outputs max-abs
+2e-3 for f16/bf16 and 3e-2 for fp8; fp8 codes and scales bit-exact.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as oa
+from oracle import fp8 as of
+from oracle import mask as om
+from paper_2606_25040_amd import ops
+from paper_2606_25040_amd import workloads as wk
+from tests.compare import compare_masks, max_abs_err
+
+pytestmark = pytest.mark.gpu
+
+TOL16 = 2e-3
+TOL8 = 3e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def device():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    ops.load_library()
+    torch.cuda.set_device(0)
+    yield
+
+
+def np64(t: torch.Tensor) -> np.ndarray:
+    return t.float().cpu().numpy()
+
+
+def rand_qkv(gen, B, S, H, dtype, scale=0.5):
+    """Random Q, K (logit std ~ scale^2) and V ~ N(0, 1).  The default keeps
+    attention diffuse like the workloads (|O| < 0.5), where the 16-bit output
+    rounding stays inside the absolute tolerance; peaked cases use
+    ``within_rounding`` instead."""
+    q = (torch.randn(B, S, H, 128, generator=gen) * scale).to(dtype)
+    k = (torch.randn(B, S, H, 128, generator=gen) * scale).to(dtype)
+    v = torch.randn(B, S, H, 128, generator=gen).to(dtype)
+    return q, k, v
+
+
+def positional_qk(B, S, H, dtype, seed):
+    """Block-structured Q/K (shared positional projection) for builder tests."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    f = np.stack([np.sin(2 * np.pi * np.arange(S) / P) for P in (37.0, 200.0, 911.0, 3000.0)] +
+                 [np.cos(2 * np.pi * np.arange(S) / P) for P in (37.0, 200.0, 911.0, 3000.0)], 1)
+    q = np.empty((B, S, H, 128), np.float32)
+    k = np.empty((B, S, H, 128), np.float32)
+    for h in range(H):
+        W = g.standard_normal((8, 128)) * 0.5
+        for b in range(B):
+            q[b, :, h] = f @ W + 0.5 * g.standard_normal((S, 128))
+            k[b, :, h] = f @ W + 0.5 * g.standard_normal((S, 128))
+    return torch.from_numpy(q).to(dtype), torch.from_numpy(k).to(dtype)
+
+
+def within_rounding(got, ref, dtype, atol=TOL16):
+    """Error bound for peaked attention where |O| can exceed 1: the absolute
+    tolerance plus one unit of the output type's relative rounding."""
+    rel = 2.0 ** -8 if dtype == torch.bfloat16 else 2.0 ** -10
+    return bool(np.all(np.abs(got - ref) <= atol + rel * np.abs(ref)))
+
+
+# --------------------------------------------------------------------------- quantiser
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
+def test_quantizer_bit_exact(dtype):
+    gen = torch.Generator().manual_seed(11)
+    B, S, H = 2, 1000, 3
+    x = torch.randn(B, S, H, 128, generator=gen) * torch.tensor([0.01, 1.0, 30.0]).view(1, 1, 3, 1)
+    x[0, 64:128, 1] = 0.0                                  # amax == 0 block
+    x[1, 128:192, 0] = -0.0
+    x[1, 192:256, 2] *= 1e-3                               # values deep in the subnormal range
+    x[0, 960:, 2] = 1e4 if dtype == torch.bfloat16 else 6e4
+    x = x.to(dtype)
+    codes, scales = ops.quantize_fp8_blockwise(x.cuda())
+    torch.cuda.synchronize()
+    oc, os_ = of.quantize_blockwise(np64(x))
+    assert np.array_equal(codes.cpu().numpy(), oc)
+    assert np.array_equal(scales.cpu().numpy(), os_)
+
+
+# --------------------------------------------------------------------------- builder
+BUILD_CASES = [(0.5, 0.05), (0.9, 0.0), (0.0, 0.3), (1.0, 0.0), (0.3, 1.0), (0.75, 0.1)]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
+def test_builder_small_all_rows(dtype):
+    B, S, H = 2, 1000, 3                                    # 16 blocks, last one 40 tokens
+    q, k = positional_qk(B, S, H, dtype, 5)
+    qd, kd = q.cuda(), k.cuda()
+    sm = 1.0 / math.sqrt(128)
+    for top_p, mk in BUILD_CASES:
+        m = ops.build_block_mask(qd, kd, top_p, mk, sm_scale=sm, return_scores=True)
+        rp, ci = m.to_host()
+        o = om.build_block_mask(np64(q), np64(k), sm, top_p, mk)
+        rep = compare_masks(rp, ci, o, range(m.rows), top_p, mk)
+        assert rep.ok, rep.failing[:5]
+        assert ops.validate_block_mask(m) == 0
+        s32 = m.block_scores.cpu().numpy()
+        assert np.array_equal(s32, o.scores.astype(np.float32)) or \
+            np.max(np.abs(s32 - o.scores) / (np.abs(o.scores) + 1e-30)) < 1.2e-7
+
+
+def test_builder_single_block_and_tiny_sequences():
+    sm = 1.0 / math.sqrt(128)
+    for S in (1, 63, 64, 65, 130):
+        q, k = positional_qk(1, S, 2, torch.bfloat16, S)
+        m = ops.build_block_mask(q.cuda(), k.cuda(), 0.6, 0.0, sm_scale=sm)
+        rp, ci = m.to_host()
+        o = om.build_block_mask(np64(q), np64(k), sm, 0.6, 0.0)
+        rep = compare_masks(rp, ci, o, range(m.rows), 0.6, 0.0)
+        assert rep.ok, (S, rep.failing[:3])
+
+
+# --------------------------------------------------------------------------- attention
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
+def test_attention_peaked_logits(dtype):
+    gen = torch.Generator().manual_seed(77)
+    B, S, H = 1, 700, 2
+    q, k, v = rand_qkv(gen, B, S, H, dtype, scale=1.6)      # logit std ~ 2.6
+    n = (S + 63) // 64
+    rng = np.random.Generator(np.random.PCG64(77))
+    rp, ci = wk.random_csr(rng, H * n, n, 0.5)
+    mask = ops.BlockMask.from_host(rp, ci, 1, H, n)
+    out = ops.block_sparse_attn_fwd(q.cuda(), k.cuda(), v.cuda(), mask)
+    O, _ = oa.attention(np64(q), np64(k), np64(v), rp, ci, 1.0 / math.sqrt(128), 1)
+    assert within_rounding(np64(out), O, dtype)
+
+
+def attn_ref_full(q, k, v, rp, ci, mask_batch, sm):
+    return oa.attention(np64(q), np64(k), np64(v), rp, ci, sm, mask_batch)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
+@pytest.mark.parametrize("S,B,H,mask_batch", [(64, 1, 1, 1), (100, 2, 2, 1), (1000, 2, 3, 2),
+                                              (1000, 2, 3, 1), (2048, 1, 2, 1)])
+def test_attention_small_full(dtype, S, B, H, mask_batch):
+    gen = torch.Generator().manual_seed(S + 7 * B + H)
+    q, k, v = rand_qkv(gen, B, S, H, dtype)
+    n = (S + 63) // 64
+    rng = np.random.Generator(np.random.PCG64(S))
+    rp, ci = wk.random_csr(rng, mask_batch * H * n, n, 0.4, empty_frac=0.1 if n > 1 else 0.0)
+    mask = ops.BlockMask.from_host(rp, ci, mask_batch, H, n)
+    sm = 1.0 / math.sqrt(128)
+    out, lse = ops.block_sparse_attn_fwd(q.cuda(), k.cuda(), v.cuda(), mask, sm_scale=sm,
+                                         return_lse=True)
+    torch.cuda.synchronize()
+    O, L = attn_ref_full(q, k, v, rp, ci, mask_batch, sm)
+    # few keys per row here, so |O| reaches ~0.7: allow the output rounding on top
+    assert within_rounding(np64(out), O, dtype)
+    lg = lse.cpu().numpy()
+    fin = np.isfinite(L)
+    assert np.array_equal(np.isfinite(lg), fin)
+    if fin.any():
+        assert np.max(np.abs(lg[fin] - L[fin])) <= 1e-3
+    # empty rows are exactly zero
+    counts = np.diff(rp)
+    for b in range(B):
+        for h in range(H):
+            for i in range(n):
+                r = oa.mask_row_index(b, h, i, H, n, mask_batch)
+                if counts[r] == 0:
+                    assert torch.all(out[b, i * 64:(i + 1) * 64, h] == 0)
+
+
+def test_attention_full_density_equals_dense_sdpa():
+    gen = torch.Generator().manual_seed(3)
+    B, S, H = 1, 777, 2
+    q, k, v = rand_qkv(gen, B, S, H, torch.bfloat16)
+    n = (S + 63) // 64
+    rp = np.arange(H * n + 1) * n
+    ci = np.tile(np.arange(n), H * n)
+    mask = ops.BlockMask.from_host(rp, ci, 1, H, n)
+    out = ops.block_sparse_attn_fwd(q.cuda(), k.cuda(), v.cuda(), mask)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        q.double().permute(0, 2, 1, 3), k.double().permute(0, 2, 1, 3),
+        v.double().permute(0, 2, 1, 3)).permute(0, 2, 1, 3)
+    assert within_rounding(np64(out), ref.numpy(), torch.bfloat16)
+
+
+def test_attention_strided_views_and_determinism():
+    gen = torch.Generator().manual_seed(9)
+    B, S, H = 2, 500, 2
+    qkv = torch.randn(B, S, 3, H, 128, generator=gen).to(torch.bfloat16).cuda()
+    q, k, v = qkv[:, :, 0], qkv[:, :, 1], qkv[:, :, 2]
+    n = (S + 63) // 64
+    rng = np.random.Generator(np.random.PCG64(1))
+    rp, ci = wk.random_csr(rng, H * n, n, 0.5)
+    mask = ops.BlockMask.from_host(rp, ci, 1, H, n)
+    o1 = ops.block_sparse_attn_fwd(q, k, v, mask)
+    o2 = ops.block_sparse_attn_fwd(q, k, v, mask)
+    order = ops.plan_block_mask(mask, B, S)
+    o3 = ops.block_sparse_attn_fwd(q, k, v, mask, schedule=order)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(o1.view(torch.int16), o3.view(torch.int16))
+    assert sorted(order.cpu().tolist()) == list(range(B * H * n))
+    O, _ = oa.attention(np64(q.cpu()), np64(k.cpu()), np64(v.cpu()), rp, ci,
+                        1.0 / math.sqrt(128), 1)
+    assert within_rounding(np64(o1), O, torch.bfloat16)
+
+
+def test_attention_fp8_small_full():
+    gen = torch.Generator().manual_seed(21)
+    B, S, H = 2, 1000, 3
+    q, k, v = rand_qkv(gen, B, S, H, torch.bfloat16)
+    n = (S + 63) // 64
+    rng = np.random.Generator(np.random.PCG64(2))
+    rp, ci = wk.random_csr(rng, H * n, n, 0.5, empty_frac=0.05)
+    mask = ops.BlockMask.from_host(rp, ci, 1, H, n)
+    qc, qs = ops.quantize_fp8_blockwise(q.cuda())
+    kc, ks = ops.quantize_fp8_blockwise(k.cuda())
+    vc, vs = ops.quantize_fp8_blockwise(v.cuda())
+    out, lse = ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs), return_lse=True)
+    torch.cuda.synchronize()
+    dq = of.dequantize_blockwise(qc.cpu().numpy(), qs.cpu().numpy())
+    dk = of.dequantize_blockwise(kc.cpu().numpy(), ks.cpu().numpy())
+    dv = of.dequantize_blockwise(vc.cpu().numpy(), vs.cpu().numpy())
+    O, L = oa.attention(dq, dk, dv, rp, ci, 1.0 / math.sqrt(128), 1)
+    assert within_rounding(np64(out), O, torch.bfloat16, atol=TOL8)
+    lg = lse.cpu().numpy()
+    fin = np.isfinite(L)
+    assert np.array_equal(np.isfinite(lg), fin)
+    if fin.any():
+        assert np.max(np.abs(lg[fin] - L[fin])) <= 1e-3
+
+
+# --------------------------------------------------------------------------- mask checker
+def test_validate_flags():
+    H, n = 2, 5
+    good_rp = np.array([0, 2, 3, 3, 5, 6, 8, 9, 9, 10, 12])
+    good_ci = np.array([0, 3, 1, 2, 4, 0, 1, 2, 3, 0, 1, 4])
+    assert ops.validate_block_mask(ops.BlockMask.from_host(good_rp, good_ci, 1, H, n)) == 0
+    bad = good_ci.copy()
+    bad[1] = 0                                              # not ascending
+    assert ops.validate_block_mask(ops.BlockMask.from_host(good_rp, bad, 1, H, n)) & 8
+    bad = good_ci.copy()
+    bad[4] = 5                                              # out of range
+    assert ops.validate_block_mask(ops.BlockMask.from_host(good_rp, bad, 1, H, n)) & 4
+    rp = good_rp.copy()
+    rp[3] = 1                                               # decreasing
+    assert ops.validate_block_mask(ops.BlockMask.from_host(rp, good_ci, 1, H, n)) & 2
+
+
+def test_abi_rejects_bad_arguments_on_device():
+    q = torch.zeros(2, 100, 2, 128, dtype=torch.bfloat16, device="cuda")
+    n = 2
+    mask = ops.BlockMask.from_host(np.arange(3 * 2 * n + 1), np.zeros(3 * 2 * n), 3, 2, n)
+    with pytest.raises(RuntimeError, match="INVALID_ARG"):
+        ops.block_sparse_attn_fwd(q, q, q, mask)
+    with pytest.raises(RuntimeError, match="INVALID_ARG"):
+        ops.build_block_mask(q, q, 1.5, 0.0)
+
+
+# --------------------------------------------------------------------------- full-size workloads
+_cache = {}
+
+
+def workload_state(key):
+    if key in _cache:
+        return _cache[key]
+    _cache.clear()
+    torch.cuda.empty_cache()
+    wl = wk.WORKLOADS[key]
+    inp = wk.make_inputs(wl)
+    st = {"wl": wl, "inp": inp}
+    q, k, v = inp.q.cuda(), inp.k.cuda(), inp.v.cuda()
+    mq, mk = inp.mask_q.cuda(), inp.mask_k.cuda()
+    mask = ops.build_block_mask(mq, mk, wl.top_p, wl.min_top_k, sm_scale=wl.sm_scale)
+    st.update(q=q, k=k, v=v, mask=mask)
+    if wl.dtype == "fp8":
+        st["q8"] = ops.quantize_fp8_blockwise(q)
+        st["k8"] = ops.quantize_fp8_blockwise(k)
+        st["v8"] = ops.quantize_fp8_blockwise(v)
+    torch.cuda.synchronize()
+    _cache[key] = st
+    return st
+
+
+FULL = ["wan5b_720p_bf16", "wan14b_480p_reuse_bf16", "wan14b_720p_fp8", "wan14b_480p_batch4_bf16"]
+
+
+@pytest.mark.parametrize("key", FULL)
+def test_full_size_mask_sampled_heads(key):
+    st = workload_state(key)
+    wl, inp, mask = st["wl"], st["inp"], st["mask"]
+    rp, ci = mask.to_host()
+    heads = sorted({0, wl.H // 2, wl.H - 1})
+    o = om.build_block_mask(inp.mask_q.float().numpy(), inp.mask_k.float().numpy(), wl.sm_scale,
+                            wl.top_p, wl.min_top_k, heads=heads)
+    n = wl.n_blocks
+    rows = [h * n + i for h in heads for i in range(n)]
+    rep = compare_masks(rp, ci, o, rows, wl.top_p, wl.min_top_k)
+    assert rep.ok, rep.failing[:5]
+    assert abs(mask.density - wl.density) < 0.01
+    assert ops.validate_block_mask(mask) == 0
+
+
+def _sample_items(wl, rng, per_head=3):
+    n = wl.n_blocks
+    items = []
+    for b in range(wl.B):
+        for h in range(wl.H):
+            picks = {0, n - 1} | set(rng.integers(0, n, size=per_head).tolist())
+            items += [(b, h, i) for i in sorted(picks)]
+    return items
+
+
+@pytest.mark.parametrize("key", FULL)
+def test_full_size_attention_sampled(key):
+    st = workload_state(key)
+    wl, mask = st["wl"], st["mask"]
+    rp, ci = mask.to_host()
+    order = ops.plan_block_mask(mask, wl.B, wl.S)
+    if wl.dtype == "fp8":
+        (qc, qs), (kc, ks), (vc, vs) = st["q8"], st["k8"], st["v8"]
+        out = ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs), schedule=order)
+        tol = TOL8
+    else:
+        out = ops.block_sparse_attn_fwd(st["q"], st["k"], st["v"], mask, schedule=order)
+        tol = TOL16
+    out2 = (ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs))
+            if wl.dtype == "fp8" else ops.block_sparse_attn_fwd(st["q"], st["k"], st["v"], mask))
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), out2.view(torch.int16))
+    rng = np.random.Generator(np.random.PCG64(wl.seed))
+    items = _sample_items(wl, rng, per_head=2 if wl.B > 1 else 3)
+    n = wl.n_blocks
+    worst = 0.0
+    by_head = {}
+    for b, h, i in items:
+        by_head.setdefault((b, h), []).append(i)
+    for (b, h), blocks in by_head.items():
+        if wl.dtype == "fp8":
+            sl = lambda c, s: of.dequantize_blockwise(c[b:b + 1, :, h:h + 1].cpu().numpy(),
+                                                      s[b:b + 1, h:h + 1].cpu().numpy())[0, :, 0]
+            qh, kh, vh = sl(qc, qs), sl(kc, ks), sl(vc, vs)
+        else:
+            qh, kh, vh = (np64(x[b, :, h].cpu()) for x in (st["q"], st["k"], st["v"]))
+        oh = np64(out[b, :, h].cpu())
+        for i in blocks:
+            r = oa.mask_row_index(b, h, i, wl.H, n, 1)
+            o_ref, _ = oa.attention_block(qh, kh, vh, oa.row_blocks(rp, ci, r), i, wl.sm_scale)
+            worst = max(worst, max_abs_err(oh[i * 64:i * 64 + o_ref.shape[0]], o_ref))
+    assert worst <= tol, worst
