@@ -1,0 +1,288 @@
+"""Benchmark of the block-sparse attention hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload KEY]
+
+A step is one pass of the whole hot path over one request batch with inputs
+resident in HBM: mask builder (block mean-pool, float64 block scores, top-p /
+top-k selection, CSR), work plan, [FP8 quantisation of Q, K, V for the fp8
+workload], and the block-sparse attention forward pass.  The metric is the
+effective TFLOP/s on computed blocks, 4 * 64 * 64 * 128 FLOP per computed
+(q-block, kv-block) pair, over the measured time.  Prints ONE JSON line.
+
+Beside the step throughput the line carries: the attention kernel's own
+throughput and MFMA-roofline fraction (HIP events on the launch stream), the
+builder time and the routing-overhead ratio routing / (routing + attention)
+(Eq. 3), the speedup over the same kernel code at 100% density, and the CPU
+oracle's throughput on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2516.6, "f16": 2516.6, "fp8": 5033.2}   # 256 CU x 2.4 GHz x 4096 / 8192
+FLOP_PER_PAIR = 4 * 64 * 64 * 128
+DEFAULT_WORKLOAD = "wan5b_720p_bf16"
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    return ap.parse_args()
+
+
+def source_hash(names) -> str:
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2606_25040_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(kernel_file: str, workload: str, src_hash: str):
+    """HBM bytes per launch from the committed counter summary, or None when
+    missing or taken on a different kernel source."""
+    path = os.path.join(PROFILES, f"traffic_{workload}.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != src_hash or rec.get("kernel_file") != kernel_file:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, inp, budget_s: float):
+    """Oracle (plain NumPy float64) on a bounded sample: the mask builder for
+    head 0 of the mask source, then attention of head 0's q-blocks in order
+    until the time budget is spent.  Returns effective TFLOP/s on computed
+    blocks and a description."""
+    from oracle import attention as oa
+    from oracle import mask as om
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = 1
+    cores = len(os.sched_getaffinity(0))
+    t0 = time.perf_counter()
+    mq = inp.mask_q[0, :, 0].float().numpy() if inp.mask_q is not None else None
+    mk = inp.mask_k[0, :, 0].float().numpy() if inp.mask_k is not None else None
+    if mq is not None:
+        s = om.block_scores(om.pool_means(mq), om.pool_means(mk), wl.sm_scale)
+        rows = [om.select_row(s[i], wl.top_p, wl.min_top_k) for i in range(wl.n_blocks)]
+    else:
+        rp, ci = inp.random_mask
+        rows = [ci[rp[i]:rp[i + 1]] for i in range(wl.n_blocks)]
+    t_build = time.perf_counter() - t0
+    if wl.dtype == "fp8":
+        from oracle import fp8 as of
+        qh, kh, vh = (of.dequantize_blockwise(*of.quantize_blockwise(x[:1, :, :1].float().numpy()))
+                      [0, :, 0] for x in (inp.q, inp.k, inp.v))
+    else:
+        qh, kh, vh = (x[0, :, 0].float().numpy() for x in (inp.q, inp.k, inp.v))
+    pairs = 0
+    done = 0
+    t1 = time.perf_counter()
+    for i in range(wl.n_blocks):
+        oa.attention_block(qh, kh, vh, rows[i], i, wl.sm_scale)
+        pairs += len(rows[i])
+        done += 1
+        if time.perf_counter() - t1 > budget_s:
+            break
+    t_attn = time.perf_counter() - t1
+    # builder share for the q-blocks covered (one head's builder serves n q-blocks)
+    t = t_attn + t_build * done / wl.n_blocks
+    value = pairs * FLOP_PER_PAIR / t / 1e12
+    sample = (f"oracle mask builder for head 0 ({wl.n_blocks} rows, {t_build:.2f} s) + oracle "
+              f"attention (gather form, float64) for q-blocks 0..{done - 1} of head 0 of request 0 "
+              f"({pairs} computed block pairs, {t_attn:.2f} s); builder time pro-rated to those "
+              f"q-blocks; float64 NumPy, BLAS threads {threads}")
+    return {"value": value, "unit": "TFLOP/s", "cores": min(threads, cores), "kind": "oracle",
+            "sample": sample}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(this build measures the single-GPU share of the path).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2606_25040_amd import ops
+    from paper_2606_25040_amd import workloads as wk
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    ops.load_library()
+    wl = wk.WORKLOADS[args.workload]
+    inp = wk.make_inputs(wl)
+    q, k, v = inp.q.cuda(), inp.k.cuda(), inp.v.cuda()
+    fp8 = wl.dtype == "fp8"
+    B, S, H = wl.B, wl.S, wl.H
+    n = wl.n_blocks
+
+    # ---- preallocated buffers: the timed region allocates nothing
+    if wl.mask_source == "random":
+        rp, ci = inp.random_mask
+        fixed = ops.BlockMask.from_host(rp, ci, 1, H, n)
+        mq = mk = None
+    else:
+        mq, mk = inp.mask_q.cuda(), inp.mask_k.cuda()
+        fixed = None
+    mask_buf = None
+    ws_build = None
+    if mq is not None:
+        Bm = mq.shape[0]
+        mask_buf = ops.BlockMask(torch.empty(Bm * H * n + 1, dtype=torch.int32, device="cuda"),
+                                 torch.empty(Bm * H * n * n, dtype=torch.int32, device="cuda"),
+                                 Bm, H, n)
+        need = ops.load_library().chorus_build_block_mask_workspace_size(
+            ops.ctypes.byref(ops.Shape(Bm, S, H, 128)))
+        ws_build = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
+    order = torch.empty(B * H * n, dtype=torch.int32, device="cuda")
+    ws_plan = torch.empty(4096 + B * H * 4, dtype=torch.uint8, device="cuda")
+    out = torch.empty((B, S, H, 128), dtype=torch.bfloat16 if fp8 else q.dtype, device="cuda")
+    if fp8:
+        codes = [torch.empty((B, S, H, 128), dtype=torch.uint8, device="cuda") for _ in range(3)]
+        scales = [torch.empty((B, H, n), dtype=torch.float32, device="cuda") for _ in range(3)]
+
+    def build():
+        if mq is None:
+            return fixed
+        return ops.build_block_mask(mq, mk, wl.top_p, wl.min_top_k, sm_scale=wl.sm_scale,
+                                    out=mask_buf, workspace=ws_build)
+
+    def plan(m):
+        return ops.plan_block_mask(m, B, S, out=order, workspace=ws_plan)
+
+    def quant():
+        for x, c, s in zip((q, k, v), codes, scales):
+            ops.quantize_fp8_blockwise(x, codes=c, scales=s)
+
+    def attn(m, sched, dense=False):
+        mm = None if dense else m
+        if fp8:
+            return ops.block_sparse_attn_fwd(codes[0], codes[1], codes[2], mm, sm_scale=wl.sm_scale,
+                                             scales=tuple(scales), out=out, schedule=sched)
+        return ops.block_sparse_attn_fwd(q, k, v, mm, sm_scale=wl.sm_scale, out=out,
+                                         schedule=sched)
+
+    def step():
+        m = build()
+        sched = plan(m)
+        if fp8:
+            quant()
+        attn(m, sched)
+
+    # ---- whole-step throughput
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    mask = build()
+    sched = plan(mask)
+    torch.cuda.synchronize()
+    nnz = mask.nnz
+    pairs = B * nnz
+    flops = pairs * FLOP_PER_PAIR
+    value = flops / (ms_per_step * 1e-3) / 1e12
+
+    # ---- per-kernel times with HIP events on the launch stream
+    def event_ms(fn, reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        e1.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    reps = max(args.steps, 10)
+    attn_ms = event_ms(lambda: attn(mask, sched), reps)
+    build_ms = event_ms(build, reps) if mq is not None else 0.0
+    plan_ms = event_ms(lambda: plan(mask), reps)
+    quant_ms = event_ms(quant, reps) if fp8 else 0.0
+    dense_reps = max(3, reps // 4)
+    dense_ms = event_ms(lambda: attn(mask, None, dense=True), dense_reps)
+    attn_tflops = flops / (attn_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[wl.dtype]
+
+    kernel_file = "attn_fwd_fp8.hip" if fp8 else "attn_fwd.hip"
+    src_hash = source_hash([kernel_file, "attn_common.h"])
+    traffic = traffic_from_profile(kernel_file, wl.key, src_hash)
+
+    line = {
+        "metric": "effective TFLOP/s on computed blocks & % MFMA peak; speedup vs 100%-density",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded Wan-class Q/K/V on the latent grid; no real latents)",
+        "config": {
+            "workload": wl.key, "B": B, "S": S, "H": H, "D": 128, "block": 64,
+            "grid_tyx": list(wl.grid), "mask_source": wl.mask_source,
+            "target_density": wl.density, "density": round(nnz / float(mask.rows * n), 5),
+            "top_p": wl.top_p, "min_top_k": wl.min_top_k, "computed_pairs": pairs,
+            "step": "mask build + plan" + (" + fp8 quantise" if fp8 else "") + " + attention",
+        },
+        "attn_ms": round(attn_ms, 4),
+        "attn_tflops": round(attn_tflops, 2),
+        "attn_frac_mfma_peak": round(attn_tflops / peak, 4),
+        "builder_ms": round(build_ms, 4),
+        "plan_ms": round(plan_ms, 4),
+        "quant_ms": round(quant_ms, 4),
+        "routing_overhead_ratio": round(build_ms / (build_ms + attn_ms), 4),
+        "dense_attn_ms": round(dense_ms, 4),
+        "speedup_vs_dense": round(dense_ms / attn_ms, 3),
+        "ideal_speedup": round(float(mask.rows * n) / nnz, 3),
+        "roofline": {
+            "kernel": ("attn_fwd_fp8_kernel<false>" if fp8 else "attn_fwd_16_kernel<true,false>"),
+            "bound": "mfma",
+            "achieved": round(attn_tflops, 2),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(attn_tflops / peak, 4),
+            "traffic": traffic,
+            "source_hash": src_hash,
+        },
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, inp, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -194,6 +194,10 @@ chorus_status chorus_quantize_fp8_blockwise(chorus_dtype in_dtype, const chorus_
  *   q_scale, k_scale, v_scale [B, H, n_blocks] (as written by the quantiser);
  *   the values read are code * scale.  QK^T and PV run as FP8 MFMA with fp32
  *   accumulation; P is rounded to e4m3 for PV.  out is bf16.
+ * mask     : the block mask; NULL means every q-block attends to every
+ *            kv-block (dense attention -- the paper's fallback when no cached
+ *            mask is available, Sec. 3.2 "Mask Caching and Retrieval"; also
+ *            the 100%-density reference of the same kernel code).
  * lse      : optional out (NULL to skip), device float32 [B, H, S] contiguous.
  * schedule : optional work order from chorus_plan_block_mask (NULL = the
  *            library's default order); never changes results.

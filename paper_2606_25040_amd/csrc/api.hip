@@ -239,7 +239,7 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   if ((st = check_tensor(k, "k", es))) return st;
   if ((st = check_tensor(v, "v", es))) return st;
   if ((st = check_tensor(out, "out", 2))) return st;
-  if ((st = check_mask(shape, mask))) return st;
+  if (mask && (st = check_mask(shape, mask))) return st;
   if (dtype == CHORUS_FP8_E4M3) {
     if (!q_scale || !k_scale || !v_scale)
       return fail(CHORUS_ERR_INVALID_ARG, "fp8 attention needs q_scale, k_scale and v_scale");
@@ -248,7 +248,7 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   }
   if (!std::isfinite(sm_scale) || !(sm_scale > 0.f))
     return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite and > 0");
-  const int n = mask->n_blocks;
+  const int n = blocks_of(shape->S);
   const int64_t items = (int64_t)shape->B * shape->H * n;
   if (items > INT32_MAX) return fail(CHORUS_ERR_UNSUPPORTED, "too many work items");
   if (schedule) {
@@ -267,15 +267,15 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   a.q_scale = q_scale;
   a.k_scale = k_scale;
   a.v_scale = v_scale;
-  a.row_ptr = mask->row_ptr;
-  a.col_idx = mask->col_idx;
+  a.row_ptr = mask ? mask->row_ptr : nullptr;   // NULL row_ptr selects the dense kernel
+  a.col_idx = mask ? mask->col_idx : nullptr;
+  a.mask_batch = mask ? mask->mask_batch : 1;
   a.order = schedule ? schedule->order : nullptr;
   a.lse = lse;
   a.B = shape->B;
   a.S = shape->S;
   a.H = shape->H;
   a.n = n;
-  a.mask_batch = mask->mask_batch;
   a.sm_scale = sm_scale;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == CHORUS_FP8_E4M3) return from_hip(launch_attn_fwd_fp8(a, s), "attn_fwd_fp8");

@@ -55,7 +55,7 @@ struct Elt<false> {
   }
 };
 
-template <bool BF16>
+template <bool BF16, bool DENSE>
 __global__ __launch_bounds__(128) void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
   using E = Elt<BF16>;
   using vec8 = typename E::vec8;
@@ -69,8 +69,14 @@ __global__ __launch_bounds__(128) void attn_fwd_16_kernel(AttnArgs a, int chunk,
   const int i = item % n;
   const int bh = item / n;
   const int h = bh % H, b = bh / H;
-  const int64_t mrow = ((int64_t)(a.mask_batch > 1 ? b : 0) * H + h) * n + i;
-  const int kb0 = a.row_ptr[mrow], kb1 = a.row_ptr[mrow + 1];
+  // DENSE: every kv block (no mask); otherwise the CSR row of (b, h, i)
+  int kb0 = 0, kb1 = n;
+  if (!DENSE) {
+    const int64_t mrow = ((int64_t)(a.mask_batch > 1 ? b : 0) * H + h) * n + i;
+    kb0 = a.row_ptr[mrow];
+    kb1 = a.row_ptr[mrow + 1];
+  }
+  auto kv_block = [&](int jj) { return DENSE ? jj : a.col_idx[jj]; };
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -120,11 +126,11 @@ __global__ __launch_bounds__(128) void attn_fwd_16_kernel(AttnArgs a, int chunk,
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[u][r] = 0.f;
 
-  int jn = kb0 < kb1 ? a.col_idx[kb0] : 0;
+  int jn = kb0 < kb1 ? kv_block(kb0) : 0;
   if (kb0 < kb1 && jn >= 0 && jn < n) load_kv(jn);
   for (int jj = kb0; jj < kb1; ++jj) {
     const int j = jn;
-    if (jj + 1 < kb1) jn = a.col_idx[jj + 1];
+    if (jj + 1 < kb1) jn = kv_block(jj + 1);
     if (j < 0 || j >= n) {           // ids outside [0, n) are skipped (the builder never emits them)
       if (jj + 1 < kb1 && jn >= 0 && jn < n) load_kv(jn);
       continue;
@@ -231,10 +237,18 @@ hipError_t launch_attn_fwd_16(chorus_dtype dt, const AttnArgs& a, hipStream_t st
   const int W = a.B * a.H * a.n;
   const int chunk = (W + kNumXcd - 1) / kNumXcd;
   const dim3 grid(chunk * kNumXcd), block(128);
-  if (dt == CHORUS_BF16)
-    hipLaunchKernelGGL(attn_fwd_16_kernel<true>, grid, block, 0, st, a, chunk, W);
-  else
-    hipLaunchKernelGGL(attn_fwd_16_kernel<false>, grid, block, 0, st, a, chunk, W);
+  const bool dense = a.row_ptr == nullptr;
+  if (dt == CHORUS_BF16) {
+    if (dense)
+      hipLaunchKernelGGL((attn_fwd_16_kernel<true, true>), grid, block, 0, st, a, chunk, W);
+    else
+      hipLaunchKernelGGL((attn_fwd_16_kernel<true, false>), grid, block, 0, st, a, chunk, W);
+  } else {
+    if (dense)
+      hipLaunchKernelGGL((attn_fwd_16_kernel<false, true>), grid, block, 0, st, a, chunk, W);
+    else
+      hipLaunchKernelGGL((attn_fwd_16_kernel<false, false>), grid, block, 0, st, a, chunk, W);
+  }
   return hipGetLastError();
 }
 

@@ -30,6 +30,7 @@ __device__ inline int k_row_of_key(int kappa) {
   return t + 8 * ((k >> 2) & 3) + 4 * (k >> 4) + (k & 3);
 }
 
+template <bool DENSE>
 __global__ __launch_bounds__(128) void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W) {
   __shared__ __attribute__((aligned(16))) uint8_t k_s[kBlock * kS8];
   __shared__ __attribute__((aligned(16))) uint8_t v_s[kBlock * kS8];
@@ -41,8 +42,13 @@ __global__ __launch_bounds__(128) void attn_fwd_fp8_kernel(AttnArgs a, int chunk
   const int i = item % n;
   const int bh = item / n;
   const int h = bh % H, b = bh / H;
-  const int64_t mrow = ((int64_t)(a.mask_batch > 1 ? b : 0) * H + h) * n + i;
-  const int kb0 = a.row_ptr[mrow], kb1 = a.row_ptr[mrow + 1];
+  int kb0 = 0, kb1 = n;
+  if (!DENSE) {
+    const int64_t mrow = ((int64_t)(a.mask_batch > 1 ? b : 0) * H + h) * n + i;
+    kb0 = a.row_ptr[mrow];
+    kb1 = a.row_ptr[mrow + 1];
+  }
+  auto kv_block = [&](int jj) { return DENSE ? jj : a.col_idx[jj]; };
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const int l32 = lane & 31, hl = lane >> 5;
@@ -53,7 +59,7 @@ __global__ __launch_bounds__(128) void attn_fwd_fp8_kernel(AttnArgs a, int chunk
   // reference V scale: the largest among the listed blocks
   float sref = 0.f;
   for (int jj = kb0 + tid; jj < kb1; jj += 128) {
-    const int j = a.col_idx[jj];
+    const int j = kv_block(jj);
     if (j >= 0 && j < n) sref = fmaxf(sref, vsc[j]);
   }
   for (int o = 32; o > 0; o >>= 1) sref = fmaxf(sref, __shfl_xor(sref, o));
@@ -107,11 +113,11 @@ __global__ __launch_bounds__(128) void attn_fwd_fp8_kernel(AttnArgs a, int chunk
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[u][r] = 0.f;
 
-  int jn = kb0 < kb1 ? a.col_idx[kb0] : 0;
+  int jn = kb0 < kb1 ? kv_block(kb0) : 0;
   if (kb0 < kb1 && jn >= 0 && jn < n) load_kv(jn);
   for (int jj = kb0; jj < kb1; ++jj) {
     const int j = jn;
-    if (jj + 1 < kb1) jn = a.col_idx[jj + 1];
+    if (jj + 1 < kb1) jn = kv_block(jj + 1);
     if (j < 0 || j >= n) {
       if (jj + 1 < kb1 && jn >= 0 && jn < n) load_kv(jn);
       continue;
@@ -225,7 +231,10 @@ __global__ __launch_bounds__(128) void attn_fwd_fp8_kernel(AttnArgs a, int chunk
 hipError_t launch_attn_fwd_fp8(const AttnArgs& a, hipStream_t st) {
   const int W = a.B * a.H * a.n;
   const int chunk = (W + kNumXcd - 1) / kNumXcd;
-  hipLaunchKernelGGL(attn_fwd_fp8_kernel, dim3(chunk * kNumXcd), dim3(128), 0, st, a, chunk, W);
+  if (a.row_ptr == nullptr)
+    hipLaunchKernelGGL(attn_fwd_fp8_kernel<true>, dim3(chunk * kNumXcd), dim3(128), 0, st, a, chunk, W);
+  else
+    hipLaunchKernelGGL(attn_fwd_fp8_kernel<false>, dim3(chunk * kNumXcd), dim3(128), 0, st, a, chunk, W);
   return hipGetLastError();
 }
 

@@ -225,14 +225,18 @@ def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: 
     return out
 
 
-def plan_block_mask(mask: BlockMask, B: int, S: int) -> torch.Tensor:
+def plan_block_mask(mask: BlockMask, B: int, S: int, out: torch.Tensor | None = None,
+                    workspace: torch.Tensor | None = None) -> torch.Tensor:
     """chorus_plan_block_mask: work order for applying ``mask`` to B requests."""
     L = load_library()
     shape = Shape(B, S, mask.H, 128)
     cm = mask.as_c()
-    order = torch.empty(B * mask.H * mask.n_blocks, dtype=torch.int32, device=mask.row_ptr.device)
+    n_items = B * mask.H * mask.n_blocks
+    order = out if out is not None else torch.empty(n_items, dtype=torch.int32,
+                                                    device=mask.row_ptr.device)
     need = L.chorus_plan_workspace_size(ctypes.byref(shape), ctypes.byref(cm))
-    ws = _workspace(need, mask.row_ptr.device)
+    ws = workspace if workspace is not None and workspace.numel() >= need + 256 else \
+        _workspace(need, mask.row_ptr.device)
     st = L.chorus_plan_block_mask(ctypes.byref(shape), ctypes.byref(cm), order.data_ptr(),
                                   _aligned(ws), need, _stream())
     _check(st, "chorus_plan_block_mask")
@@ -267,13 +271,14 @@ def quantize_fp8_blockwise(x: torch.Tensor, codes: torch.Tensor | None = None,
     return codes, scales
 
 
-def block_sparse_attn_fwd(q, k, v, mask: BlockMask, sm_scale: float | None = None,
+def block_sparse_attn_fwd(q, k, v, mask: BlockMask | None, sm_scale: float | None = None,
                           scales=None, out: torch.Tensor | None = None, return_lse: bool = False,
                           schedule: torch.Tensor | None = None):
     """chorus_block_sparse_attn_fwd (dtype taken from q: f16, bf16 or uint8 fp8 codes).
 
-    ``scales`` = (q_scale, k_scale, v_scale) for fp8 codes.  Returns ``out``
-    (and ``lse [B, H, S]`` fp32 when ``return_lse``).
+    ``scales`` = (q_scale, k_scale, v_scale) for fp8 codes; ``mask=None`` runs
+    every block pair (dense attention).  Returns ``out`` (and ``lse [B, H, S]``
+    fp32 when ``return_lse``).
     """
     L = load_library()
     dt = _dtype_code(q)
@@ -289,15 +294,15 @@ def block_sparse_attn_fwd(q, k, v, mask: BlockMask, sm_scale: float | None = Non
             raise ValueError("fp8 attention needs (q_scale, k_scale, v_scale)")
         qs, ks, vs = (s.data_ptr() for s in scales)
     shape = _shape(q)
-    cm = mask.as_c()
+    cm = ctypes.byref(mask.as_c()) if mask is not None else None
     sched = None
     if schedule is not None:
         sched = ctypes.byref(Schedule(schedule.data_ptr(), schedule.numel()))
-    need = L.chorus_attn_workspace_size(dt, ctypes.byref(shape), ctypes.byref(cm))
+    need = L.chorus_attn_workspace_size(dt, ctypes.byref(shape), cm)
     ws = _workspace(need, q.device)
     st = L.chorus_block_sparse_attn_fwd(dt, ctypes.byref(shape), ctypes.byref(_tensor(q)),
                                         ctypes.byref(_tensor(k)), ctypes.byref(_tensor(v)), qs, ks,
-                                        vs, ctypes.byref(cm), sched, sm, ctypes.byref(_tensor(out)),
+                                        vs, cm, sched, sm, ctypes.byref(_tensor(out)),
                                         _ptr(lse), _aligned(ws), need, _stream())
     _check(st, "chorus_block_sparse_attn_fwd")
     return (out, lse) if return_lse else out
