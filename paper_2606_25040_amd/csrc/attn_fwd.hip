@@ -2,32 +2,44 @@
 // block-sparse kernel": only the listed block pairs enter QK^T, softmax, PV).
 //
 // One workgroup = one work item (request b, head h, 64-query block i), two
-// waves of 32 queries.  For each listed kv block j (64 keys):
-//   * K_j and V_j are staged global -> registers -> LDS; the next block's
-//     global loads are issued before the current block is computed;
+// waves of 32 queries, 32 KB of LDS, so four workgroups (two waves per SIMD)
+// share a CU and hide each other's latencies.  For each listed kv block j:
+//   * K_j and V_j go global -> LDS with global_load_lds_dwordx4 (no register
+//     staging); each tile has its own single buffer, refilled as soon as the
+//     phase that reads it is over (K after QK^T, V after PV), so the next
+//     block's loads overlap this block's softmax and PV;
 //   * S^T = K_j Q^T with v_mfma_f32_32x32x16 (A = K rows from LDS, B = Q
-//     fragments kept in registers), so each lane holds 32 scores of ONE query
-//     (lane l and l ^ 32 split that query's 64 keys): row max and row sum are
+//     fragments kept in registers): each lane holds 32 scores of ONE query
+//     (lanes l and l ^ 32 split its 64 keys), so the row max and row sum are
 //     lane-local plus one half-wave exchange;
-//   * online softmax in the log2 domain (exp2, scale folded into one multiply);
-//   * O^T += V_j^T P^T with the same MFMA; V^T fragments come straight from
-//     the row-major LDS tile through ds_read_b64_tr_b16, and the P fragment is
-//     the score accumulator itself converted to 16-bit, so P never leaves
-//     registers.
+//   * online softmax in the log2 domain; the running max is only moved (and
+//     O, l rescaled) when some row's max grew by more than kRescaleLog2, so
+//     P <= 2^kRescaleLog2 and most blocks skip the 64-register rescale;
+//   * O^T += V_j^T P^T with the same MFMA; V^T fragments come from the
+//     row-major tile through ds_read_b64_tr_b16; P is the score accumulator
+//     converted to 16-bit in registers.
+// LDS tiles are XOR-swizzled in 16-byte chunks (the direct loads permute the
+// global addresses instead of the LDS ones) so that the b128 K reads and the
+// transposed b64 V reads are bank-conflict free.
 // Epilogue: O = O^T / l written as 16-bit, lse = ln(sum exp) in fp32.
 #include "attn_common.h"
 
 namespace chorus {
 namespace {
 
-constexpr int kKS = 136;  // K tile row stride in 16-bit elements (272 B: conflict-free b128 reads)
-constexpr int kVS = 144;  // V tile row stride (288 B: conflict-free transposed b64 reads)
+constexpr float kRescaleLog2 = 8.f;
+constexpr int kTileBytes = kBlock * kHeadDim * 2;   // 16 KB per 16-bit tile
+
+// 16-byte chunk position of chunk c in row r.
+__device__ inline int k_swz(int r, int c) { return c ^ (r & 15); }
+__device__ inline int v_swz_bits(int r) { return (0xE4A0 >> (4 * (r & 3))) & 15; }   // {0, 10, 4, 14}
+__device__ inline int v_swz(int r, int c) { return c ^ v_swz_bits(r); }
 
 template <bool BF16>
 struct Elt;
-// The transposed LDS reads are issued through the typed builtins and joined
-// with __builtin_shufflevector: assembling the operand element by element
-// from the i16 variant was miscompiled (lanes received repeated elements).
+// The transposed LDS reads go through the typed builtin (or a whole-vector
+// bitcast) and are joined with __builtin_shufflevector: assembling the
+// operand element by element from the i16 variant was miscompiled.
 template <>
 struct Elt<true> {
   using vec8 = bf16x8;
@@ -35,7 +47,7 @@ struct Elt<true> {
   static __device__ inline f32x16 mfma(vec8 a, vec8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
-  static __device__ inline vec8 tr_pair(const uint16_t* lo, const uint16_t* hi) {
+  static __device__ inline vec8 tr_pair(const char* lo, const char* hi) {
     const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)lo);
     const bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)hi);
     return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -48,20 +60,75 @@ struct Elt<false> {
   static __device__ inline f32x16 mfma(vec8 a, vec8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
   }
-  static __device__ inline vec8 tr_pair(const uint16_t* lo, const uint16_t* hi) {
+  static __device__ inline vec8 tr_pair(const char* lo, const char* hi) {
     const f16x4 a = __builtin_bit_cast(f16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)lo));
     const f16x4 b = __builtin_bit_cast(f16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)hi));
     return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
   }
 };
 
+// One global -> LDS direct load (16 bytes per lane, lane-linear destination
+// at `lds`): inline asm so that the compiler does not drain every pending
+// load before each LDS read (it cannot tell which tile a DMA writes); the
+// kernel waits on the vector-memory counter itself.
+__device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
+               : "memory", "m0");
+}
+
+// This wave's share of one 64 x 128 16-bit tile: instruction u fills LDS rows
+// 8u + 4 wave .. + 3 (1 KB, lane-linear), each lane fetching the global chunk
+// that the swizzle places at its slot.  Full blocks take the row offset from
+// the scalar base and a per-lane offset fixed for the whole kernel; the
+// partial last block clamps rows past the sequence end to row S - 1 (their
+// keys are masked and their probabilities are zero).
+struct TileLoader {
+  const char* base;    // token 0 of this (b, h)
+  uint32_t ss;         // token stride in bytes
+  uint32_t off[2];     // lane offset for even / odd u (row r0, swizzled chunk)
+  int r0, p;
+  template <bool IS_K>
+  __device__ void init(const uint16_t* b, int64_t stride, int wave, int lane) {
+    base = reinterpret_cast<const char*>(b);
+    ss = (uint32_t)(stride * 2);
+    r0 = 4 * wave + (lane >> 4);
+    p = lane & 15;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int c = IS_K ? k_swz(r0 + 8 * e, p) : v_swz(r0 + 8 * e, p);
+      off[e] = (uint32_t)r0 * ss + (uint32_t)c * 16;
+    }
+  }
+  template <bool IS_K>
+  __device__ void load(char* tile, int j, int S, int wave) const {
+    const uint32_t lds = (uint32_t)(size_t)(__attribute__((address_space(3))) char*)tile + wave * 1024;
+    if (j * kBlock + kBlock <= S) {
+      const char* rowj = base + (int64_t)j * kBlock * ss;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) dma16(lds + u * 2048, rowj + (int64_t)(8 * u) * ss, off[u & 1]);
+    } else {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int r = 8 * u + r0;
+        const int c = IS_K ? k_swz(r, p) : v_swz(r, p);
+        const int tok = min(j * kBlock + r, S - 1);
+        dma16(lds + u * 2048, base, (uint32_t)tok * ss + (uint32_t)c * 16);
+      }
+    }
+  }
+};
+
+// Wait until at most n vector-memory loads of this wave are outstanding.
+#define CHORUS_WAIT_VMCNT(n) asm volatile("s_waitcnt vmcnt(" #n ")" ::: "memory")
+
 template <bool BF16, bool DENSE>
-__global__ __launch_bounds__(128) void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
   using E = Elt<BF16>;
   using vec8 = typename E::vec8;
   using scalar = typename E::scalar;
-  __shared__ __attribute__((aligned(16))) uint16_t k_s[kBlock * kKS];
-  __shared__ __attribute__((aligned(16))) uint16_t v_s[kBlock * kVS];
+  __shared__ __attribute__((aligned(1024))) char k_s[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char v_s[kTileBytes];
 
   const int item = work_item(a.order, chunk, W);
   if (item < 0) return;
@@ -77,10 +144,34 @@ __global__ __launch_bounds__(128) void attn_fwd_16_kernel(AttnArgs a, int chunk,
     kb1 = a.row_ptr[mrow + 1];
   }
   auto kv_block = [&](int jj) { return DENSE ? jj : a.col_idx[jj]; };
+  // ids outside [0, n) are skipped (the builder never emits them)
+  auto next_valid = [&](int jj) {
+    while (jj < kb1) {
+      const int j = kv_block(jj);
+      if (j >= 0 && j < n) break;
+      ++jj;
+    }
+    return jj;
+  };
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+  const int lane = tid & 63;
   const int l32 = lane & 31, hl = lane >> 5;
+  const int g = lane >> 4, j16 = lane & 15;
+
+  const uint16_t* kbase = static_cast<const uint16_t*>(a.k.data) + (int64_t)b * a.k.sb + (int64_t)h * a.k.sh;
+  const uint16_t* vbase = static_cast<const uint16_t*>(a.v.data) + (int64_t)b * a.v.sb + (int64_t)h * a.v.sh;
+
+  TileLoader kl, vl;
+  kl.init<true>(kbase, a.k.ss, wave, lane);
+  vl.init<false>(vbase, a.v.ss, wave, lane);
+  int jj = next_valid(kb0);
+  if (jj < kb1) {
+    const int j0 = kv_block(jj);
+    kl.load<true>(k_s, j0, S, wave);
+    vl.load<false>(v_s, j0, S, wave);
+  }
 
   // Q^T fragments: query qrow, head-dim slice 16 s + 8 hl .. + 8
   const int qrow = i * kBlock + wave * 32 + l32;
@@ -98,25 +189,16 @@ __global__ __launch_bounds__(128) void attn_fwd_16_kernel(AttnArgs a, int chunk,
       }
     }
   }
+  // Drain the Q loads (and the first tiles) with an s_waitcnt the compiler
+  // sees, so that it does not re-wait for Q inside the loop.
+  __builtin_amdgcn_s_waitcnt(0xF70);   // vmcnt(0)
 
-  const uint16_t* kbase = static_cast<const uint16_t*>(a.k.data) + (int64_t)b * a.k.sb + (int64_t)h * a.k.sh;
-  const uint16_t* vbase = static_cast<const uint16_t*>(a.v.data) + (int64_t)b * a.v.sb + (int64_t)h * a.v.sh;
-  const int srow = tid >> 4;          // staging: rows srow + 8 u, 16-byte column chunk scol
-  const int scol = (tid & 15) * 8;
-  uint4 kreg[8], vreg[8];
-  auto load_kv = [&](int j) {
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int tok = j * kBlock + srow + 8 * u;
-      if (tok < S) {
-        kreg[u] = *reinterpret_cast<const uint4*>(kbase + (int64_t)tok * a.k.ss + scol);
-        vreg[u] = *reinterpret_cast<const uint4*>(vbase + (int64_t)tok * a.v.ss + scol);
-      } else {
-        kreg[u] = make_uint4(0, 0, 0, 0);
-        vreg[u] = make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
+  // per-lane LDS byte offsets of the K (A operand) and V^T (transposed) reads
+  const int k_row_off = l32 * 256;
+  const int k_swzl = l32 & 15;
+  const int v_lane_off = (j16 >> 2) * 256 + 8 * (j16 & 1);
+  const int v_c0 = 2 * (g & 1) + ((j16 & 3) >> 1);
+  const int v_sl = v_swz_bits(j16 >> 2);
 
   const float cl2 = a.sm_scale * kLog2e;
   float m_run = -INFINITY, l_run = 0.f;
@@ -126,35 +208,32 @@ __global__ __launch_bounds__(128) void attn_fwd_16_kernel(AttnArgs a, int chunk,
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[u][r] = 0.f;
 
-  int jn = kb0 < kb1 ? kv_block(kb0) : 0;
-  if (kb0 < kb1 && jn >= 0 && jn < n) load_kv(jn);
-  for (int jj = kb0; jj < kb1; ++jj) {
-    const int j = jn;
-    if (jj + 1 < kb1) jn = kv_block(jj + 1);
-    if (j < 0 || j >= n) {           // ids outside [0, n) are skipped (the builder never emits them)
-      if (jj + 1 < kb1 && jn >= 0 && jn < n) load_kv(jn);
-      continue;
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      *reinterpret_cast<uint4*>(k_s + (srow + 8 * u) * kKS + scol) = kreg[u];
-      *reinterpret_cast<uint4*>(v_s + (srow + 8 * u) * kVS + scol) = vreg[u];
-    }
-    __syncthreads();
-    if (jj + 1 < kb1 && jn >= 0 && jn < n) load_kv(jn);
+  while (jj < kb1) {
+    const int j = kv_block(jj);
+    const int jn = next_valid(jj + 1);
+    const bool has_next = jn < kb1;
+    const int j_next = has_next ? kv_block(jn) : 0;
 
-    // S^T tiles t = 0, 1 (keys 32 t .. 32 t + 31) x 32 queries
+    // K_j resident: at most this block's V loads (8) are still in flight
+    CHORUS_WAIT_VMCNT(8);
+    __syncthreads();
     f32x16 sacc[2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) sacc[t][r] = 0.f;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const vec8 kf = *reinterpret_cast<const vec8*>(k_s + (32 * t + l32) * kKS + 16 * s + 8 * hl);
+    for (int s = 0; s < 8; ++s) {
+      const int koff = k_row_off + (((2 * s + hl) ^ k_swzl) << 4);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {       // two independent accumulation chains
+        const vec8 kf = *reinterpret_cast<const vec8*>(k_s + t * 32 * 256 + koff);
         sacc[t] = E::mfma(kf, qf[s], sacc[t]);
       }
     }
+    __syncthreads();                               // every wave is done with K_j
+    if (has_next) kl.load<true>(k_s, j_next, S, wave);
+
     // keys at or beyond S (partial last block) carry no weight
     if (j * kBlock + kBlock > S) {
 #pragma unroll
@@ -172,40 +251,52 @@ __global__ __launch_bounds__(128) void attn_fwd_16_kernel(AttnArgs a, int chunk,
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[t][r]);
     mx = pair_max(mx);
     const float m_new = fmaxf(m_run, mx * cl2);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    if (__builtin_amdgcn_ballot_w64(m_new > m_run + kRescaleLog2) != 0) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[u][r] *= alpha;
+    }
     float rs = 0.f;
     vec8 pf[2][2];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(sacc[t][r] * cl2 - m_new);
+        const float p = __builtin_amdgcn_exp2f(sacc[t][r] * cl2 - m_run);
         rs += p;
         pf[t][r >> 3][r & 7] = (scalar)p;
       }
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[u][r] *= alpha;
+    l_run += rs;
 
-    // O^T[u] += V^T[u] P^T: k-slot i of lane half hl maps to key
-    // 32 t + 16 hh + 8 (i / 4) + 4 hl + i % 4 in both operands.
-    const int g = lane >> 4, j16 = lane & 15;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int n0 = 32 * u + 16 * (g & 1) + 4 * (j16 & 3);
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int k0 = 32 * t + 16 * hh + 4 * (g >> 1) + (j16 >> 2);
-          const vec8 vf = E::tr_pair(v_s + k0 * kVS + n0, v_s + (k0 + 8) * kVS + n0);
-          o[u] = E::mfma(vf, pf[t][hh], o[u]);
-        }
+    // V_j resident: only the next K tile's loads (8, if issued) may be in flight
+    if (has_next) {
+      CHORUS_WAIT_VMCNT(8);
+    } else {
+      CHORUS_WAIT_VMCNT(0);
     }
     __syncthreads();
+    // O^T[u] += V^T[u] P^T: k-slot i of lane half hl maps to key
+    // 32 t + 16 hh + 8 (i / 4) + 4 hl + i % 4 in both operands.
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int k0 = 32 * t + 16 * hh + 4 * (g >> 1);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {     // four independent accumulators
+          const int cu = (4 * u + v_c0) ^ v_sl;
+          const char* lo = v_s + k0 * 256 + v_lane_off + (cu << 4);
+          const vec8 vf = E::tr_pair(lo, lo + 8 * 256);
+          o[u] = E::mfma(vf, pf[t][hh], o[u]);
+        }
+      }
+    __syncthreads();                               // every wave is done with V_j
+    if (has_next) vl.load<false>(v_s, j_next, S, wave);
+    jj = jn;
   }
 
   // epilogue: lane pair (l, l ^ 32) holds partial sums of the same query
