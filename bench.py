@@ -160,7 +160,7 @@ def main():
         need = ops.load_library().chorus_build_block_mask_workspace_size(
             ops.ctypes.byref(ops.Shape(Bm, S, H, 128)))
         ws_build = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
-    order = torch.empty(B * H * n, dtype=torch.int32, device="cuda")
+    order = torch.empty(B * H, dtype=torch.int32, device="cuda")
     ws_plan = torch.empty(4096 + B * H * 4, dtype=torch.uint8, device="cuda")
     out = torch.empty((B, S, H, 128), dtype=torch.bfloat16 if fp8 else q.dtype, device="cuda")
     if fp8:

@@ -91,10 +91,11 @@ typedef struct {
   const int32_t* col_idx;   /* [nnz] ascending kv-block ids per row             */
 } chorus_block_mask;
 
-/* Optional work order for the attention kernels (see chorus_plan_block_mask). */
+/* Optional work order for the attention kernels (see chorus_plan_block_mask):
+ * the order in which the (request, head) units are dealt to the XCDs. */
 typedef struct {
-  const int32_t* order;     /* [B * H * n_blocks] permutation of work items     */
-  int32_t n_items;          /* must equal B * H * n_blocks                       */
+  const int32_t* order;     /* [B * H] permutation of units u = b * H + h       */
+  int32_t n_units;          /* must equal B * H                                  */
 } chorus_schedule;
 
 /* ---------------------------------------------------------------------------
@@ -139,15 +140,18 @@ chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* sh
 /* ---------------------------------------------------------------------------
  * Work plan -- the one-GPU counterpart of the paper's head-level scheduling
  * (Sec. 3.2 "Head-level scheduling for load balancing", Appendix A): because
- * a reused mask's per-head cost is known before the attention runs, the work
- * can be placed ahead of time.  Here the work items (b, h, i) of one attention
- * call are split into 8 contiguous runs of near-equal cost (cost = listed
- * blocks + 1), one per XCD, and written interleaved so that dispatch position
- * p runs on XCD p mod 8; within an XCD items keep their (b, h, i) order so
- * neighbouring q-blocks of one head share L2.  Computed on device, once per
- * mask, and reusable for every call that applies the same mask to B requests.
+ * a reused mask's per-head cost is known before the attention runs, heads can
+ * be placed ahead of time.  The attention kernels deal their work to the 8
+ * XCDs of the GPU in 8 equal runs of (request, head) units; the plan orders
+ * the units so that those runs carry near-equal cost: units are taken
+ * heaviest first (cost = listed blocks + q-blocks) and each goes to the
+ * least-loaded XCD that still has room, the paper's greedy rule with the XCDs
+ * in the role of the GPUs.  Within an XCD units keep ascending id, so the
+ * workgroups running together share one head's K/V in that XCD's L2.
+ * Computed on device, once per mask, and reusable for every call that applies
+ * the same mask to B requests.
  *
- * order         : out, device int32 [B * H * n_blocks] (a permutation).
+ * order         : out, device int32 [B * H] (a permutation of b * H + h).
  * workspace     : device scratch of chorus_plan_workspace_size() bytes.
  * The plan only changes performance, never results.
  * ------------------------------------------------------------------------- */

@@ -1,6 +1,7 @@
 // Host side of the C ABI: argument validation, workspace carving, dispatch.
 // Nothing here allocates device memory or synchronises; all work is enqueued
 // on the caller's stream.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -251,11 +252,13 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   const int n = blocks_of(shape->S);
   const int64_t items = (int64_t)shape->B * shape->H * n;
   if (items > INT32_MAX) return fail(CHORUS_ERR_UNSUPPORTED, "too many work items");
+  if ((int64_t)(n - 1) * kBlock * std::max(std::max(q->stride_s, k->stride_s), v->stride_s) * 2 > UINT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "token stride too large for 32-bit in-head offsets");
   if (schedule) {
     if (!schedule->order) return fail(CHORUS_ERR_INVALID_ARG, "schedule order is NULL");
-    if (schedule->n_items != items)
-      return fail(CHORUS_ERR_INVALID_ARG, "schedule has %d items, expected %lld", schedule->n_items,
-                  (long long)items);
+    if (schedule->n_units != shape->B * shape->H)
+      return fail(CHORUS_ERR_INVALID_ARG, "schedule has %d units, expected B*H = %d", schedule->n_units,
+                  shape->B * shape->H);
   }
   if ((st = check_workspace(workspace, workspace_bytes, chorus_attn_workspace_size(dtype, shape, mask))))
     return st;

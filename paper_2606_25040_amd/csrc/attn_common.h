@@ -33,15 +33,88 @@ __device__ inline float pair_sum(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Work item of dispatch slot p: slots are dealt round-robin to the 8 XCDs, so
-// slot p runs on XCD p % 8; XCD x walks positions [x * chunk, (x + 1) * chunk)
-// of the (optionally planned) item order.  Returns -1 for idle slots.
-__device__ inline int work_item(const int32_t* order, int chunk, int W) {
+// Work item of dispatch slot p.  Items are pairs of neighbouring q-blocks,
+// `np` per (request, head) unit, numbered unit * np + pair.  Slots are dealt
+// round-robin to the 8 XCDs, so slot p runs on XCD p % 8; XCD x walks item
+// positions [x * chunk, (x + 1) * chunk) of the unit order (the planned
+// order of (request, head) units, or the natural one).  Returns -1 for idle
+// slots.
+__device__ inline int work_item(const int32_t* order, int chunk, int W, int np) {
   const int p = blockIdx.x;
   const int pos = (p % kNumXcd) * chunk + p / kNumXcd;
   if (pos >= W) return -1;
-  const int item = order ? order[pos] : pos;
-  return (item >= 0 && item < W) ? item : -1;
+  if (!order) return pos;
+  const int unit = order[pos / np];
+  const int item = unit * np + pos % np;
+  return (unit >= 0 && item < W) ? item : -1;
 }
+
+// One global -> LDS direct load (16 bytes per lane, lane-linear destination
+// at `lds`, a wave-uniform LDS byte address): inline asm so that the compiler
+// does not drain every pending load before each LDS read (it cannot tell
+// which tile a direct load writes); kernels wait on the vector-memory
+// counter themselves.
+__device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
+               : "memory", "m0");
+}
+
+// Wait until at most n vector-memory loads of this wave are outstanding.
+#define CHORUS_WAIT_VMCNT(n) asm volatile("s_waitcnt vmcnt(" #n ")" ::: "memory")
+
+// Walk of the merged kv lists of the two q-blocks (2p, 2p + 1) of a pair in
+// ascending kv id, skipping ids outside [0, n).  All lanes hold the same
+// state (it lives in scalar registers).
+struct PairWalk {
+  const int32_t* col;
+  int pa, a1, pb, b1, n;
+  bool dense;
+  __device__ void init(const AttnArgs& a, bool is_dense, int b, int h, int ip) {
+    col = a.col_idx;
+    n = a.n;
+    dense = is_dense;
+    const int ia = 2 * ip, ib = 2 * ip + 1;
+    if (dense) {
+      pa = 0;
+      a1 = n;
+      pb = 0;
+      b1 = ib < n ? n : 0;
+    } else {
+      const int64_t r0 = ((int64_t)(a.mask_batch > 1 ? b : 0) * a.H + h) * n;
+      pa = a.row_ptr[r0 + ia];
+      a1 = a.row_ptr[r0 + ia + 1];
+      pb = ib < n ? a.row_ptr[r0 + ib] : 0;
+      b1 = ib < n ? a.row_ptr[r0 + ib + 1] : 0;
+    }
+  }
+  __device__ bool listed(int sel) const { return sel == 0 ? a1 > pa : b1 > pb; }
+  __device__ int id_at(int p) const { return dense ? p : col[p]; }
+  __device__ int head_a() {
+    while (pa < a1) {
+      const int j = id_at(pa);
+      if (j >= 0 && j < n) return j;
+      ++pa;
+    }
+    return INT32_MAX;
+  }
+  __device__ int head_b() {
+    while (pb < b1) {
+      const int j = id_at(pb);
+      if (j >= 0 && j < n) return j;
+      ++pb;
+    }
+    return INT32_MAX;
+  }
+  // next kv block of the union (INT32_MAX when done) and which q-blocks list it
+  __device__ int next(bool& in_a, bool& in_b) {
+    const int ja = head_a(), jb = head_b();
+    const int j = min(ja, jb);
+    in_a = ja == j && j != INT32_MAX;
+    in_b = jb == j && j != INT32_MAX;
+    if (in_a) ++pa;
+    if (in_b) ++pb;
+    return j;
+  }
+};
 
 }  // namespace chorus

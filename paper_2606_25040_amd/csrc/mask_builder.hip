@@ -309,11 +309,11 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// 5. Work plan: head units (b, h) with cost sum_i (blocks(b,h,i) + 1) are
-// assigned to the 8 XCDs greedily, heaviest first, each to the least-loaded
-// XCD that still has room (equal unit counts per XCD); the order lists the
-// units XCD by XCD (ascending unit id inside an XCD), each expanded to its
-// q-blocks in order.  One workgroup.
+// 5. Work plan: head units u = b * H + h with cost sum_i (blocks(b,h,i) + 1)
+// are assigned to the 8 XCDs greedily, heaviest first, each to the
+// least-loaded XCD that still has room (equal unit counts per XCD); the order
+// lists the units XCD by XCD, ascending unit id inside an XCD.  One
+// workgroup; beyond kPlanMaxUnits units the natural order is kept.
 // ---------------------------------------------------------------------------
 constexpr int kPlanMaxUnits = 4096;
 
@@ -329,55 +329,46 @@ __global__ __launch_bounds__(256) void plan_kernel(const int32_t* __restrict__ r
     unit_cost[u] = row_ptr[r0 + n] - row_ptr[r0] + n;
   }
   __syncthreads();
-  if (tid == 0) {
-    if (U > kPlanMaxUnits) {
-      // too many units for the greedy pass: keep the natural order
-    } else {
-      // sort unit ids by (cost desc, id asc): insertion sort into unit_order
-      for (int u = 0; u < U; ++u) {
-        const int32_t cu = unit_cost[u];
-        int p = u;
-        while (p > 0) {
-          const int prev = unit_order[p - 1];
-          const int32_t cp = unit_cost[prev];
-          if (cp > cu || (cp == cu && prev < u)) break;
-          unit_order[p] = prev;
-          --p;
-        }
-        unit_order[p] = u;
+  if (tid == 0 && U <= kPlanMaxUnits) {
+    // unit ids by (cost desc, id asc): insertion sort
+    for (int u = 0; u < U; ++u) {
+      const int32_t cu = unit_cost[u];
+      int p = u;
+      while (p > 0) {
+        const int prev = unit_order[p - 1];
+        const int32_t cp = unit_cost[prev];
+        if (cp > cu || (cp == cu && prev < u)) break;
+        unit_order[p] = prev;
+        --p;
       }
-      int64_t load[kNumXcd];
-      int used[kNumXcd], cap[kNumXcd];
-      for (int x = 0; x < kNumXcd; ++x) {
-        load[x] = 0;
-        used[x] = 0;
-        cap[x] = U / kNumXcd + (x < U % kNumXcd ? 1 : 0);
-      }
-      // assignment stored temporarily in unit_cost (cost no longer needed after read)
-      for (int p = 0; p < U; ++p) {
-        const int u = unit_order[p];
-        int best = -1;
-        for (int x = 0; x < kNumXcd; ++x) {
-          if (used[x] >= cap[x]) continue;
-          if (best < 0 || load[x] < load[best]) best = x;
-        }
-        load[best] += unit_cost[u];
-        used[best] += 1;
-        unit_cost[u] = -1 - best;
-      }
-      int p = 0;
-      for (int x = 0; x < kNumXcd; ++x)
-        for (int u = 0; u < U; ++u)
-          if (unit_cost[u] == -1 - x) unit_order[p++] = u;
+      unit_order[p] = u;
     }
+    int64_t load[kNumXcd];
+    int used[kNumXcd], cap[kNumXcd];
+    for (int x = 0; x < kNumXcd; ++x) {
+      load[x] = 0;
+      used[x] = 0;
+      cap[x] = U / kNumXcd + (x < U % kNumXcd ? 1 : 0);
+    }
+    // the assignment overwrites unit_cost (each cost is read before)
+    for (int p = 0; p < U; ++p) {
+      const int u = unit_order[p];
+      int best = -1;
+      for (int x = 0; x < kNumXcd; ++x) {
+        if (used[x] >= cap[x]) continue;
+        if (best < 0 || load[x] < load[best]) best = x;
+      }
+      load[best] += unit_cost[u];
+      used[best] += 1;
+      unit_cost[u] = -1 - best;
+    }
+    int p = 0;
+    for (int x = 0; x < kNumXcd; ++x)
+      for (int u = 0; u < U; ++u)
+        if (unit_cost[u] == -1 - x) unit_order[p++] = u;
   }
   __syncthreads();
-  const int64_t W = (int64_t)U * n;
-  for (int64_t w = tid; w < W; w += 256) {
-    const int slot = (int)(w / n), i = (int)(w % n);
-    const int u = U > kPlanMaxUnits ? slot : unit_order[slot];
-    order[w] = u * n + i;
-  }
+  for (int u = tid; u < U; u += 256) order[u] = U > kPlanMaxUnits ? u : unit_order[u];
 }
 
 // ---------------------------------------------------------------------------

@@ -43,7 +43,7 @@ class Mask(ctypes.Structure):
 
 
 class Schedule(ctypes.Structure):
-    _fields_ = [("order", ctypes.c_void_p), ("n_items", ctypes.c_int32)]
+    _fields_ = [("order", ctypes.c_void_p), ("n_units", ctypes.c_int32)]
 
 
 EXPORTS = [
@@ -227,12 +227,12 @@ def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: 
 
 def plan_block_mask(mask: BlockMask, B: int, S: int, out: torch.Tensor | None = None,
                     workspace: torch.Tensor | None = None) -> torch.Tensor:
-    """chorus_plan_block_mask: work order for applying ``mask`` to B requests."""
+    """chorus_plan_block_mask: (request, head) unit order for applying ``mask``
+    to B requests (int32 [B * H])."""
     L = load_library()
     shape = Shape(B, S, mask.H, 128)
     cm = mask.as_c()
-    n_items = B * mask.H * mask.n_blocks
-    order = out if out is not None else torch.empty(n_items, dtype=torch.int32,
+    order = out if out is not None else torch.empty(B * mask.H, dtype=torch.int32,
                                                     device=mask.row_ptr.device)
     need = L.chorus_plan_workspace_size(ctypes.byref(shape), ctypes.byref(cm))
     ws = workspace if workspace is not None and workspace.numel() >= need + 256 else \

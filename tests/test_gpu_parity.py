@@ -209,7 +209,7 @@ def test_attention_strided_views_and_determinism():
     torch.cuda.synchronize()
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
     assert torch.equal(o1.view(torch.int16), o3.view(torch.int16))
-    assert sorted(order.cpu().tolist()) == list(range(B * H * n))
+    assert sorted(order.cpu().tolist()) == list(range(B * H))
     O, _ = oa.attention(np64(q.cpu()), np64(k.cpu()), np64(v.cpu()), rp, ci,
                         1.0 / math.sqrt(128), 1)
     assert within_rounding(np64(o1), O, torch.bfloat16)
