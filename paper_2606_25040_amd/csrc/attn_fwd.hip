@@ -1,17 +1,13 @@
 // Block-sparse attention forward, fp16 / bf16 (Chorus II Sec. 3.2 "Efficient
 // block-sparse kernel": only the listed block pairs enter QK^T, softmax, PV).
 //
-// Work item = a PAIR of neighbouring 64-query blocks (2p, 2p + 1) of one
-// (request, head); four waves of 32 queries (waves 0-1: block 2p, waves 2-3:
-// block 2p + 1).  Neighbouring q-blocks list mostly the same kv blocks, so the
-// workgroup walks the merged (union) list and stages each K/V tile once for
-// both; a wave whose q-block does not list the current kv block skips its
-// arithmetic.  Tiles are double-buffered in LDS (2 x 32 KB per workgroup, two
-// workgroups = two waves per SIMD per CU): the loads of the next kv block are
-// issued right after the single barrier of an iteration and have the whole
-// iteration to land.
-//
-// Per kv block j and wave:
+// One workgroup = one work item (request b, head h, 64-query block i), two
+// waves of 32 queries, 32 KB of LDS, so four workgroups (two waves per SIMD)
+// share a CU and hide each other's latencies.  For each listed kv block j:
+//   * K_j and V_j go global -> LDS with global_load_lds_dwordx4 (no register
+//     staging); each tile has its own single buffer, refilled as soon as the
+//     phase that reads it is over (K after QK^T, V after PV), so the next
+//     block's loads overlap this block's softmax and PV;
 //   * S^T = K_j Q^T with v_mfma_f32_32x32x16 (A = K rows from LDS, B = Q
 //     fragments kept in registers): each lane holds 32 scores of ONE query
 //     (lanes l and l ^ 32 split its 64 keys), so the row max and row sum are
@@ -22,9 +18,8 @@
 //   * O^T += V_j^T P^T with the same MFMA; V^T fragments come from the
 //     row-major tile through ds_read_b64_tr_b16; P is the score accumulator
 //     converted to 16-bit in registers.
-// K/V move global -> LDS with global_load_lds_dwordx4 (no register staging);
-// the tiles are XOR-swizzled in 16-byte chunks (the loads permute the global
-// addresses, the LDS side stays lane-linear) so that the b128 K reads and the
+// LDS tiles are XOR-swizzled in 16-byte chunks (the direct loads permute the
+// global addresses instead of the LDS ones) so that the b128 K reads and the
 // transposed b64 V reads are bank-conflict free.
 // Epilogue: O = O^T / l written as 16-bit, lse = ln(sum exp) in fp32.
 #include "attn_common.h"
@@ -34,7 +29,6 @@ namespace {
 
 constexpr float kRescaleLog2 = 8.f;
 constexpr int kTileBytes = kBlock * kHeadDim * 2;   // 16 KB per 16-bit tile
-constexpr int kWaves = 4;
 
 // 16-byte chunk position of chunk c in row r.
 __device__ inline int k_swz(int r, int c) { return c ^ (r & 15); }
@@ -74,15 +68,15 @@ struct Elt<false> {
 };
 
 // This wave's share of one 64 x 128 16-bit tile: instruction u fills LDS rows
-// 16u + 4 wave .. + 3 (1 KB, lane-linear), each lane fetching the global
-// chunk that the swizzle places at its slot.  Full blocks take the row offset
-// from the scalar base and a per-lane offset fixed for the whole kernel; the
+// 8u + 4 wave .. + 3 (1 KB, lane-linear), each lane fetching the global chunk
+// that the swizzle places at its slot.  Full blocks take the row offset from
+// the scalar base and a per-lane offset fixed for the whole kernel; the
 // partial last block clamps rows past the sequence end to row S - 1 (their
 // keys are masked and their probabilities are zero).
 struct TileLoader {
   const char* base;    // token 0 of this (b, h)
   uint32_t ss;         // token stride in bytes
-  uint32_t off;        // lane offset (row r0, swizzled chunk)
+  uint32_t off[2];     // lane offset for even / odd u (row r0, swizzled chunk)
   int r0, p;
   template <bool IS_K>
   __device__ void init(const uint16_t* b, int64_t stride, int wave, int lane) {
@@ -90,79 +84,92 @@ struct TileLoader {
     ss = (uint32_t)(stride * 2);
     r0 = 4 * wave + (lane >> 4);
     p = lane & 15;
-    const int c = IS_K ? k_swz(r0, p) : v_swz(r0, p);
-    off = (uint32_t)r0 * ss + (uint32_t)c * 16;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int c = IS_K ? k_swz(r0 + 8 * e, p) : v_swz(r0 + 8 * e, p);
+      off[e] = (uint32_t)r0 * ss + (uint32_t)c * 16;
+    }
   }
   template <bool IS_K>
-  __device__ void load(uint32_t lds, int j, int S, int wave) const {
-    lds += wave * 1024;
+  __device__ void load(char* tile, int j, int S, int wave) const {
+    const uint32_t lds = (uint32_t)(size_t)(__attribute__((address_space(3))) char*)tile + wave * 1024;
     if (j * kBlock + kBlock <= S) {
       const char* rowj = base + (int64_t)j * kBlock * ss;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) dma16(lds + u * 4096, rowj + (int64_t)(16 * u) * ss, off);
+      for (int u = 0; u < 8; ++u) dma16(lds + u * 2048, rowj + (int64_t)(8 * u) * ss, off[u & 1]);
     } else {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int r = 16 * u + r0;
+      for (int u = 0; u < 8; ++u) {
+        const int r = 8 * u + r0;
         const int c = IS_K ? k_swz(r, p) : v_swz(r, p);
         const int tok = min(j * kBlock + r, S - 1);
-        dma16(lds + u * 4096, base, (uint32_t)tok * ss + (uint32_t)c * 16);
+        dma16(lds + u * 2048, base, (uint32_t)tok * ss + (uint32_t)c * 16);
       }
     }
   }
 };
 
 template <bool BF16, bool DENSE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
-void attn_fwd_16_kernel(AttnArgs a, int chunk, int W, int np) {
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
   using E = Elt<BF16>;
   using vec8 = typename E::vec8;
   using scalar = typename E::scalar;
-  __shared__ __attribute__((aligned(1024))) char tiles[2][2][kTileBytes];   // [buffer][K, V]
+  __shared__ __attribute__((aligned(1024))) char k_s[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char v_s[kTileBytes];
 
-  const int item = work_item(a.order, chunk, W, np);
+  const int item = work_item(a.order, chunk, W, a.n);
   if (item < 0) return;
   const int n = a.n, H = a.H, S = a.S;
-  const int ip = item % np;
-  const int bh = item / np;
+  const int i = item % n;
+  const int bh = item / n;
   const int h = bh % H, b = bh / H;
+  // DENSE: every kv block (no mask); otherwise the CSR row of (b, h, i)
+  int kb0 = 0, kb1 = n;
+  if (!DENSE) {
+    const int64_t mrow = ((int64_t)(a.mask_batch > 1 ? b : 0) * H + h) * n + i;
+    kb0 = a.row_ptr[mrow];
+    kb1 = a.row_ptr[mrow + 1];
+  }
+  auto kv_block = [&](int jj) { return DENSE ? jj : a.col_idx[jj]; };
+  // ids outside [0, n) are skipped (the builder never emits them)
+  auto next_valid = [&](int jj) {
+    while (jj < kb1) {
+      const int j = kv_block(jj);
+      if (j >= 0 && j < n) break;
+      ++jj;
+    }
+    return jj;
+  };
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int lane = tid & 63;
   const int l32 = lane & 31, hl = lane >> 5;
   const int g = lane >> 4, j16 = lane & 15;
-  const int sel = wave >> 1;                  // 0: q-block 2p, 1: q-block 2p + 1
-  const int i = 2 * ip + sel;
-  const bool q_active = i < n;
-
-  PairWalk walk;
-  walk.init(a, DENSE, b, h, ip);
-  const bool listed_any = q_active && walk.listed(sel);
 
   const uint16_t* kbase = static_cast<const uint16_t*>(a.k.data) + (int64_t)b * a.k.sb + (int64_t)h * a.k.sh;
   const uint16_t* vbase = static_cast<const uint16_t*>(a.v.data) + (int64_t)b * a.v.sb + (int64_t)h * a.v.sh;
+
   TileLoader kl, vl;
   kl.init<true>(kbase, a.k.ss, wave, lane);
   vl.init<false>(vbase, a.v.ss, wave, lane);
-  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) char*)&tiles[0][0][0];
-
-  bool in_a, in_b;
-  int j = walk.next(in_a, in_b);
-  if (j != INT32_MAX) {
-    kl.load<true>(lds0, j, S, wave);
-    vl.load<false>(lds0 + kTileBytes, j, S, wave);
+  int jj = next_valid(kb0);
+  if (jj < kb1) {
+    const int j0 = kv_block(jj);
+    kl.load<true>(k_s, j0, S, wave);
+    vl.load<false>(v_s, j0, S, wave);
   }
 
   // Q^T fragments: query qrow, head-dim slice 16 s + 8 hl .. + 8
-  const int qrow = i * kBlock + (wave & 1) * 32 + l32;
+  const int qrow = i * kBlock + wave * 32 + l32;
   vec8 qf[8];
   {
     const uint16_t* qp = static_cast<const uint16_t*>(a.q.data) + (int64_t)b * a.q.sb + (int64_t)qrow * a.q.ss +
                          (int64_t)h * a.q.sh + 8 * hl;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
-      if (q_active && qrow < S) {
+      if (qrow < S) {
         qf[s] = *reinterpret_cast<const vec8*>(qp + 16 * s);
       } else {
 #pragma unroll
@@ -189,100 +196,102 @@ void attn_fwd_16_kernel(AttnArgs a, int chunk, int W, int np) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[u][r] = 0.f;
 
-  int buf = 0;
-  while (j != INT32_MAX) {
-    const bool mine = sel == 0 ? in_a : in_b;
-    bool na, nb;
-    const int jn = walk.next(na, nb);
-    // this block's tiles have landed in every wave; the other buffer is free
-    CHORUS_WAIT_VMCNT(0);
+  while (jj < kb1) {
+    const int j = kv_block(jj);
+    const int jn = next_valid(jj + 1);
+    const bool has_next = jn < kb1;
+    const int j_next = has_next ? kv_block(jn) : 0;
+
+    // K_j resident: at most this block's V loads (8) are still in flight
+    CHORUS_WAIT_VMCNT(8);
     __syncthreads();
-    if (jn != INT32_MAX) {
-      const uint32_t nxt = lds0 + (buf ^ 1) * 2 * kTileBytes;
-      kl.load<true>(nxt, jn, S, wave);
-      vl.load<false>(nxt + kTileBytes, jn, S, wave);
+    f32x16 sacc[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[t][r] = 0.f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const int koff = k_row_off + (((2 * s + hl) ^ k_swzl) << 4);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {       // two independent accumulation chains
+        const vec8 kf = *reinterpret_cast<const vec8*>(k_s + t * 32 * 256 + koff);
+        sacc[t] = E::mfma(kf, qf[s], sacc[t]);
+      }
     }
-    if (mine && q_active) {
-      const char* k_s = &tiles[buf][0][0];
-      const char* v_s = &tiles[buf][1][0];
-      f32x16 sacc[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[t][r] = 0.f;
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const int koff = k_row_off + (((2 * s + hl) ^ k_swzl) << 4);
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {       // two independent accumulation chains
-          const vec8 kf = *reinterpret_cast<const vec8*>(k_s + t * 32 * 256 + koff);
-          sacc[t] = E::mfma(kf, qf[s], sacc[t]);
-        }
-      }
-      // keys at or beyond S (partial last block) carry no weight
-      if (j * kBlock + kBlock > S) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
-            if (j * kBlock + key >= S) sacc[t][r] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[t][r]);
-      mx = pair_max(mx);
-      const float m_new = fmaxf(m_run, mx * cl2);
-      if (__builtin_amdgcn_ballot_w64(m_new > m_run + kRescaleLog2) != 0) {
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[u][r] *= alpha;
-      }
-      float rs = 0.f;
-      vec8 pf[2][2];
+    __syncthreads();                               // every wave is done with K_j
+    if (has_next) kl.load<true>(k_s, j_next, S, wave);
+
+    // keys at or beyond S (partial last block) carry no weight
+    if (j * kBlock + kBlock > S) {
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(sacc[t][r] * cl2 - m_run);
-          rs += p;
-          pf[t][r >> 3][r & 7] = (scalar)p;
-        }
-      l_run += rs;
-      // O^T[u] += V^T[u] P^T: k-slot i of lane half hl maps to key
-      // 32 t + 16 hh + 8 (i / 4) + 4 hl + i % 4 in both operands.
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int k0 = 32 * t + 16 * hh + 4 * (g >> 1);
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {     // four independent accumulators
-            const int cu = (4 * u + v_c0) ^ v_sl;
-            const char* lo = v_s + k0 * 256 + v_lane_off + (cu << 4);
-            const vec8 vf = E::tr_pair(lo, lo + 8 * 256);
-            o[u] = E::mfma(vf, pf[t][hh], o[u]);
-          }
+          const int key = 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
+          if (j * kBlock + key >= S) sacc[t][r] = -INFINITY;
         }
     }
-    j = jn;
-    in_a = na;
-    in_b = nb;
-    buf ^= 1;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[t][r]);
+    mx = pair_max(mx);
+    const float m_new = fmaxf(m_run, mx * cl2);
+    if (__builtin_amdgcn_ballot_w64(m_new > m_run + kRescaleLog2) != 0) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[u][r] *= alpha;
+    }
+    float rs = 0.f;
+    vec8 pf[2][2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = __builtin_amdgcn_exp2f(sacc[t][r] * cl2 - m_run);
+        rs += p;
+        pf[t][r >> 3][r & 7] = (scalar)p;
+      }
+    l_run += rs;
+
+    // V_j resident: only the next K tile's loads (8, if issued) may be in flight
+    if (has_next) {
+      CHORUS_WAIT_VMCNT(8);
+    } else {
+      CHORUS_WAIT_VMCNT(0);
+    }
+    __syncthreads();
+    // O^T[u] += V^T[u] P^T: k-slot i of lane half hl maps to key
+    // 32 t + 16 hh + 8 (i / 4) + 4 hl + i % 4 in both operands.
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int k0 = 32 * t + 16 * hh + 4 * (g >> 1);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {     // four independent accumulators
+          const int cu = (4 * u + v_c0) ^ v_sl;
+          const char* lo = v_s + k0 * 256 + v_lane_off + (cu << 4);
+          const vec8 vf = E::tr_pair(lo, lo + 8 * 256);
+          o[u] = E::mfma(vf, pf[t][hh], o[u]);
+        }
+      }
+    __syncthreads();                               // every wave is done with V_j
+    if (has_next) vl.load<false>(v_s, j_next, S, wave);
+    jj = jn;
   }
 
   // epilogue: lane pair (l, l ^ 32) holds partial sums of the same query
   const float l_tot = pair_sum(l_run);
-  const bool live = listed_any && l_tot > 0.f;
+  const bool live = kb1 > kb0 && l_tot > 0.f;
   const float inv_l = live ? 1.f / l_tot : 0.f;
-  if (q_active && qrow < S) {
+  if (qrow < S) {
     uint16_t* op = static_cast<uint16_t*>(const_cast<void*>(a.o.data)) + (int64_t)b * a.o.sb +
                    (int64_t)qrow * a.o.ss + (int64_t)h * a.o.sh;
 #pragma unroll
@@ -304,21 +313,20 @@ void attn_fwd_16_kernel(AttnArgs a, int chunk, int W, int np) {
 }  // namespace
 
 hipError_t launch_attn_fwd_16(chorus_dtype dt, const AttnArgs& a, hipStream_t st) {
-  const int np = (a.n + 1) / 2;
-  const int W = a.B * a.H * np;
+  const int W = a.B * a.H * a.n;
   const int chunk = (W + kNumXcd - 1) / kNumXcd;
-  const dim3 grid(chunk * kNumXcd), block(64 * kWaves);
+  const dim3 grid(chunk * kNumXcd), block(128);
   const bool dense = a.row_ptr == nullptr;
   if (dt == CHORUS_BF16) {
     if (dense)
-      hipLaunchKernelGGL((attn_fwd_16_kernel<true, true>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_16_kernel<true, true>), grid, block, 0, st, a, chunk, W);
     else
-      hipLaunchKernelGGL((attn_fwd_16_kernel<true, false>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_16_kernel<true, false>), grid, block, 0, st, a, chunk, W);
   } else {
     if (dense)
-      hipLaunchKernelGGL((attn_fwd_16_kernel<false, true>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_16_kernel<false, true>), grid, block, 0, st, a, chunk, W);
     else
-      hipLaunchKernelGGL((attn_fwd_16_kernel<false, false>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_16_kernel<false, false>), grid, block, 0, st, a, chunk, W);
   }
   return hipGetLastError();
 }
