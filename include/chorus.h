@@ -152,7 +152,9 @@ chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* sh
  * the same mask to B requests.
  *
  * order         : out, device int32 [B * H] (a permutation of b * H + h).
- * workspace     : device scratch of chorus_plan_workspace_size() bytes.
+ * workspace     : device scratch of chorus_plan_workspace_size() bytes; the
+ *                 current plan needs none (size 0, NULL accepted).
+ * Units beyond 4096 (B * H > 4096) keep the natural order.
  * The plan only changes performance, never results.
  * ------------------------------------------------------------------------- */
 size_t chorus_plan_workspace_size(const chorus_shape* shape, const chorus_block_mask* mask);

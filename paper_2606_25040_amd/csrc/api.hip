@@ -167,9 +167,9 @@ chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* sh
 }
 
 size_t chorus_plan_workspace_size(const chorus_shape* shape, const chorus_block_mask* mask) {
+  (void)shape;
   (void)mask;
-  if (!shape || shape->B < 1 || shape->H < 1) return 0;
-  return align_up((size_t)shape->B * shape->H * sizeof(int32_t), 256);
+  return 0;   // the plan runs in LDS
 }
 
 chorus_status chorus_plan_block_mask(const chorus_shape* shape, const chorus_block_mask* mask,
@@ -181,8 +181,8 @@ chorus_status chorus_plan_block_mask(const chorus_shape* shape, const chorus_blo
   if ((st = check_mask(shape, mask))) return st;
   if (!order) return fail(CHORUS_ERR_INVALID_ARG, "order is NULL");
   if ((st = check_workspace(workspace, workspace_bytes, chorus_plan_workspace_size(shape, mask)))) return st;
-  return from_hip(launch_plan(mask->row_ptr, mask->mask_batch, shape->B, shape->H, mask->n_blocks,
-                              static_cast<int32_t*>(workspace), order, static_cast<hipStream_t>(stream)),
+  return from_hip(launch_plan(mask->row_ptr, mask->mask_batch, shape->B, shape->H, mask->n_blocks, order,
+                              static_cast<hipStream_t>(stream)),
                   "plan");
 }
 

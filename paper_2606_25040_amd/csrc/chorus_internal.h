@@ -61,8 +61,8 @@ hipError_t launch_score_select(const double* qbar, const double* kbar, int B, in
 hipError_t launch_scan_counts(const int32_t* counts, int64_t rows, int32_t* row_ptr, hipStream_t st);
 hipError_t launch_compact(const uint32_t* bitmap, int words, const int32_t* row_ptr, int64_t rows,
                           int32_t* col_idx, hipStream_t st);
-hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n,
-                       int32_t* unit_cost_ws, int32_t* order, hipStream_t st);
+hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n, int32_t* order,
+                       hipStream_t st);
 hipError_t launch_validate(const int32_t* row_ptr, const int32_t* col_idx, int64_t rows, int n,
                            int64_t capacity, int32_t* flags, hipStream_t st);
 

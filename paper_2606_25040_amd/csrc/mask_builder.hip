@@ -122,18 +122,31 @@ __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ q
 }
 
 // ---------------------------------------------------------------------------
-// 2b. Per-row selection.  One workgroup per mask row:
-//   load the row's n scores into LDS (padded to a power of two with -inf),
-//   max and sum of exp in float64, bitonic sort by (score desc, index asc),
-//   mass in sorted order, inclusive scan, k_p = 1 + first position whose
-//   cumulative mass reaches top_p, k = min(n, max(k_p, k_min, 1)), and a
-//   bitmap of the first k indices.
+// 2b. Per-row selection.  One workgroup per mask row; thread t owns blocks
+// j = t + 256 e.  The kept set is the first k blocks of the order (score
+// descending, index ascending), k = min(n, max(k_p, k_min, 1)).  It is found
+// without sorting the row: the position k is the first one at which both
+// conditions hold -- cumulative mass >= top_p (dropped when top_p <= 0) and
+// position >= max(k_min, 1) -- and both are monotone along the order, so a
+// radix descent over an order-preserving 64-bit image of the float64 scores
+// finds the block at that position: per 8-bit digit, a histogram of block
+// counts and masses over the candidates, then the digit whose cumulative
+// (count, mass), counted from the top, first meets both conditions becomes
+// the new candidate range.  The descent stops when that digit holds a single
+// block; blocks with bit-identical scores left after all 64 bits are ordered
+// by index.  Masses enter the histograms as 62-bit fixed-point integers so
+// every sum is exact and independent of the order of the atomic adds: the
+// selection is deterministic.
 // ---------------------------------------------------------------------------
 constexpr int kSelThreads = 256;
+constexpr double kMassOne = 4611686018427387904.0;          // 2^62
+static_assert(kSelThreads == 256, "one histogram bin per thread");
 
-__device__ inline bool before(double ka, int ia, double kb, int ib) {
-  // true if (ka, ia) comes first in (score desc, index asc) order
-  return ka > kb || (ka == kb && ia < ib);
+// Order-preserving image of a float64 (larger score -> larger key); -0 is
+// folded onto +0 so equal scores give equal keys.
+__device__ inline uint64_t order_key(double s) {
+  const uint64_t u = (uint64_t)__double_as_longlong(s == 0.0 ? 0.0 : s);
+  return (u >> 63) ? ~u : (u | (1ull << 63));
 }
 
 __device__ double block_reduce_max(double v, double* red) {
@@ -158,92 +171,258 @@ __device__ double block_reduce_sum(double v, double* red) {
   return r;
 }
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(const double* __restrict__ scores, int n, int N,
+__device__ uint64_t block_reduce_sum_u64(uint64_t v, uint64_t* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  uint64_t r = red[0];
+  for (int i = 1; i < kSelThreads / 64; ++i) r += red[i];
+  return r;
+}
+
+struct SelCond {
+  uint64_t target;   // ceil(top_p * 2^62)
+  uint32_t kk;       // max(k_min, 1)
+  bool any_mass;     // top_p <= 0: the mass condition always holds
+  __device__ bool operator()(uint32_t cnt, uint64_t mass) const {
+    return cnt >= kk && (any_mass || mass >= target);
+  }
+};
+
+__device__ uint64_t block_reduce_min_u64(uint64_t v, uint64_t* red) {
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t w = __shfl_xor(v, o);
+    v = w < v ? w : v;
+  }
+  const int wv = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[wv] = v;
+  __syncthreads();
+  uint64_t r = red[0];
+  for (int i = 1; i < kSelThreads / 64; ++i) r = red[i] < r ? red[i] : r;
+  return r;
+}
+
+__device__ uint64_t block_reduce_max_u64(uint64_t v, uint64_t* red) {
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t w = __shfl_xor(v, o);
+    v = w > v ? w : v;
+  }
+  const int wv = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[wv] = v;
+  __syncthreads();
+  uint64_t r = red[0];
+  for (int i = 1; i < kSelThreads / 64; ++i) r = red[i] > r ? red[i] : r;
+  return r;
+}
+
+// Dynamic LDS: key[n] and mass[n] (uint64 each).
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const double* __restrict__ scores, int n,
                                                              double top_p, int k_min,
                                                              int32_t* __restrict__ counts,
                                                              uint32_t* __restrict__ bitmap, int words) {
-  extern __shared__ double smem[];
-  double* key = smem;                                        // [N]
-  int* idx = reinterpret_cast<int*>(key + N);                // [N]
-  double* part = reinterpret_cast<double*>(idx + N);         // [kSelThreads]
-  double* red = part + kSelThreads;                          // [4]
-  uint32_t* bits = reinterpret_cast<uint32_t*>(red + 4);     // [N / 32]
-  __shared__ int kp_min;
+  extern __shared__ uint64_t sel_smem[];
+  uint64_t* key = sel_smem;
+  uint64_t* mass = sel_smem + n;
+  __shared__ uint32_t hist_cnt[256];
+  __shared__ uint64_t hist_mass[256];
+  __shared__ uint32_t bits[kMaxBuilderBlocks / 32];
+  __shared__ uint32_t ties[kMaxBuilderBlocks / 32];
+  __shared__ double red[kSelThreads / 64];
+  __shared__ uint64_t red64[kSelThreads / 64];
+  __shared__ uint64_t sel_mass_above, tie_mass, bound_key;
+  __shared__ uint32_t sel_cnt_above, sel_bin, sel_bin_cnt;
+  __shared__ int bound_j;
+
   const int64_t row = blockIdx.x;
   const double* s = scores + row * n;
-  const int tid = threadIdx.x;
-  for (int j = tid; j < N; j += kSelThreads) {
-    key[j] = j < n ? s[j] : -INFINITY;
-    idx[j] = j;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  for (int w = tid; w < words; w += kSelThreads) {
+    bits[w] = 0u;
+    ties[w] = 0u;
   }
-  for (int w = tid; w < N / 32; w += kSelThreads) bits[w] = 0u;
-  if (tid == 0) kp_min = n;
+  // scores -> row max -> exp -> row sum -> fixed-point masses and keys
   double m = -INFINITY;
-  for (int j = tid; j < n; j += kSelThreads) m = fmax(m, s[j]);
+  for (int j = tid; j < n; j += kSelThreads) {
+    const double v = s[j];
+    key[j] = order_key(v);
+    m = fmax(m, v);
+  }
   m = block_reduce_max(m, red);
   double z = 0.0;
-  for (int j = tid; j < n; j += kSelThreads) z += exp(s[j] - m);
+  for (int j = tid; j < n; j += kSelThreads) {
+    const double x = exp(s[j] - m);
+    mass[j] = (uint64_t)__double_as_longlong(x);
+    z += x;
+  }
   z = block_reduce_sum(z, red);
-  __syncthreads();
-  // bitonic sort: the final order is ascending in the `before` relation
-  for (int size = 2; size <= N; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int t = tid; t < N / 2; t += kSelThreads) {
-        const int lo = 2 * t - (t & (stride - 1));
-        const int hi = lo + stride;
-        const bool up = (lo & size) == 0;
-        const double ka = key[lo], kb = key[hi];
-        const int ia = idx[lo], ib = idx[hi];
-        const bool swap = up ? before(kb, ib, ka, ia) : before(ka, ia, kb, ib);
-        if (swap) {
-          key[lo] = kb; key[hi] = ka;
-          idx[lo] = ib; idx[hi] = ia;
+  uint64_t total = 0, kmin = ~0ull, kmax = 0;
+  for (int j = tid; j < n; j += kSelThreads) {
+    const uint64_t q = __double2ull_rn(__longlong_as_double((long long)mass[j]) / z * kMassOne);
+    mass[j] = q;
+    total += q;
+    const uint64_t kj = key[j];
+    kmin = kj < kmin ? kj : kmin;
+    kmax = kj > kmax ? kj : kmax;
+  }
+  total = block_reduce_sum_u64(total, red64);
+  kmin = block_reduce_min_u64(kmin, red64);
+  kmax = block_reduce_max_u64(kmax, red64);
+
+  SelCond cond;
+  cond.any_mass = !(top_p > 0.0);
+  cond.target = cond.any_mass ? 0 : (uint64_t)ceil(fmin(top_p, 1.0) * kMassOne);
+  cond.kk = (uint32_t)(k_min > 1 ? k_min : 1);
+  // k = n when top_p >= 1, when the floor reaches n, or when rounding keeps
+  // the whole row's mass below top_p
+  const bool keep_all = top_p >= 1.0 || cond.kk >= (uint32_t)n || !cond((uint32_t)n, total);
+
+  uint64_t kb = 0;   // keep blocks with key > kb, and key == kb with index <= jb
+  int jb = n;
+  uint32_t k = (uint32_t)n;
+  if (!keep_all) {
+    // Descent state: every candidate agrees with `prefix` on bits >= lo; the
+    // bits above the highest one in which the row's keys differ are common
+    // to all blocks, so the descent starts below them.
+    const uint64_t diff = kmin ^ kmax;
+    int lo = diff ? 64 - __clzll((long long)diff) : 0;
+    uint64_t prefix = lo == 64 ? 0 : (kmin >> lo) << lo;
+    uint64_t mass_above = 0;
+    uint32_t cnt_above = 0, bin_cnt = (uint32_t)n;
+    while (lo > 0) {
+      const int shift = lo > 8 ? lo - 8 : 0;
+      hist_cnt[tid] = 0u;
+      hist_mass[tid] = 0ull;
+      __syncthreads();
+      for (int j = tid; j < n; j += kSelThreads) {
+        const uint64_t kj = key[j];
+        if (lo == 64 || ((kj ^ prefix) >> lo) == 0) {
+          const int bin = (int)((kj >> shift) & 255);
+          atomicAdd(&hist_cnt[bin], 1u);
+          atomicAdd((unsigned long long*)&hist_mass[bin], (unsigned long long)mass[j]);
         }
       }
       __syncthreads();
-    }
-  }
-  // cumulative mass in sorted order: each thread scans a contiguous chunk
-  const int per = N / kSelThreads > 0 ? N / kSelThreads : 1;
-  const int c0 = tid * per;
-  double local = 0.0;
-  for (int r = c0; r < c0 + per && r < N; ++r) local += r < n ? exp(key[r] - m) / z : 0.0;
-  part[tid] = local;
-  __syncthreads();
-  if (tid == 0) {
-    double run = 0.0;
-    for (int t = 0; t < kSelThreads; ++t) {
-      const double v = part[t];
-      part[t] = run;
-      run += v;
-    }
-  }
-  __syncthreads();
-  int kp;
-  if (top_p <= 0.0) {
-    kp = 0;
-  } else if (top_p >= 1.0) {
-    kp = n;
-  } else {
-    double run = part[tid];
-    for (int r = c0; r < c0 + per && r < n; ++r) {
-      run += exp(key[r] - m) / z;
-      if (run >= top_p) {
-        atomicMin(&kp_min, r + 1);
-        break;
+      if (wave == 0) {
+        // lane l owns bins 4l .. 4l+3; the bins above them are lanes > l
+        uint32_t c[4], c4 = 0;
+        uint64_t ms[4], m4 = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          c[q] = hist_cnt[4 * lane + q];
+          ms[q] = hist_mass[4 * lane + q];
+          c4 += c[q];
+          m4 += ms[q];
+        }
+        uint32_t cs = c4;
+        uint64_t msum = m4;
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t vc = __shfl_down(cs, o);
+          const uint64_t vm = __shfl_down(msum, o);
+          if (lane + o < 64) {
+            cs += vc;
+            msum += vm;
+          }
+        }
+        uint32_t cc = cnt_above + (cs - c4);
+        uint64_t mm = mass_above + (msum - m4);
+        bool before = cond(cc, mm);
+#pragma unroll
+        for (int q = 3; q >= 0; --q) {
+          const uint32_t c2 = cc + c[q];
+          const uint64_t m2 = mm + ms[q];
+          const bool now = cond(c2, m2);
+          if (now && !before) {
+            sel_bin = (uint32_t)(4 * lane + q);
+            sel_cnt_above = cc;
+            sel_mass_above = mm;
+            sel_bin_cnt = c[q];
+          }
+          before = now;
+          cc = c2;
+          mm = m2;
+        }
       }
+      __syncthreads();
+      prefix = (prefix & ~(255ull << shift)) | ((uint64_t)sel_bin << shift);
+      cnt_above = sel_cnt_above;
+      mass_above = sel_mass_above;
+      bin_cnt = sel_bin_cnt;
+      lo = shift;
+      if (bin_cnt == 1) break;
     }
-    __syncthreads();
-    kp = kp_min;
+    if (bin_cnt == 1) {
+      // the boundary block is the only candidate left
+      for (int j = tid; j < n; j += kSelThreads) {
+        const uint64_t kj = key[j];
+        if (lo == 64 || ((kj ^ prefix) >> lo) == 0) {
+          bound_key = kj;
+          bound_j = j;
+        }
+      }
+      __syncthreads();
+      kb = bound_key;
+      jb = bound_j;
+      k = cnt_above + 1;
+    } else {
+      // bin_cnt blocks share the score `prefix` (and so one mass): the
+      // boundary is the t-th of them in index order
+      for (int j = tid; j < n; j += kSelThreads) {
+        if (key[j] == prefix) {
+          atomicOr(&ties[j >> 5], 1u << (j & 31));
+          tie_mass = mass[j];   // identical for every tied block
+        }
+      }
+      __syncthreads();
+      uint32_t t = 1;
+      if (!cond.any_mass && mass_above < cond.target && tie_mass > 0)
+        t = (uint32_t)((cond.target - mass_above + tie_mass - 1) / tie_mass);
+      if (cond.kk > cnt_above && cond.kk - cnt_above > t) t = cond.kk - cnt_above;
+      if (t > bin_cnt) t = bin_cnt;
+      if (wave == 0) {
+        // lane l owns tie words 2l, 2l+1 (words <= 128)
+        const uint32_t w0 = 2 * lane < words ? ties[2 * lane] : 0u;
+        const uint32_t w1 = 2 * lane + 1 < words ? ties[2 * lane + 1] : 0u;
+        const uint32_t cnt = __popc(w0) + __popc(w1);
+        uint32_t incl = cnt;
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t v = __shfl_up(incl, o);
+          if (lane >= o) incl += v;
+        }
+        const uint32_t excl = incl - cnt;
+        if (excl < t && t <= incl) {
+          uint32_t r = t - excl;   // r-th set bit of (w0, w1), 1-based
+          int j = -1;
+          for (int b = 0; b < 64; ++b) {
+            const uint32_t wv = b < 32 ? w0 : w1;
+            if ((wv >> (b & 31)) & 1u) {
+              if (--r == 0) {
+                j = 64 * lane + b;
+                break;
+              }
+            }
+          }
+          bound_j = j;
+        }
+      }
+      __syncthreads();
+      kb = prefix;
+      jb = bound_j;
+      k = cnt_above + t;
+    }
   }
-  int k = kp > k_min ? kp : k_min;
-  if (k < 1) k = 1;
-  if (k > n) k = n;
-  for (int r = tid; r < k; r += kSelThreads) atomicOr(&bits[idx[r] >> 5], 1u << (idx[r] & 31));
+  for (int j = tid; j < n; j += kSelThreads) {
+    const uint64_t kj = key[j];
+    if (keep_all || kj > kb || (kj == kb && j <= jb)) atomicOr(&bits[j >> 5], 1u << (j & 31));
+  }
   __syncthreads();
   uint32_t* dst = bitmap + row * words;
   for (int w = tid; w < words; w += kSelThreads) dst[w] = bits[w];
-  if (tid == 0) counts[row] = k;
+  if (tid == 0) counts[row] = (int32_t)k;
 }
 
 // ---------------------------------------------------------------------------
@@ -313,36 +492,40 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict
 // are assigned to the 8 XCDs greedily, heaviest first, each to the
 // least-loaded XCD that still has room (equal unit counts per XCD); the order
 // lists the units XCD by XCD, ascending unit id inside an XCD.  One
-// workgroup; beyond kPlanMaxUnits units the natural order is kept.
+// workgroup, everything in LDS: costs, a rank sort by (cost desc, id asc),
+// then the sequential greedy pass.  Beyond kPlanMaxUnits units the natural
+// order is kept.
 // ---------------------------------------------------------------------------
 constexpr int kPlanMaxUnits = 4096;
 
 __global__ __launch_bounds__(256) void plan_kernel(const int32_t* __restrict__ row_ptr, int mask_batch, int B,
-                                                   int H, int n, int32_t* __restrict__ unit_cost,
-                                                   int32_t* __restrict__ order) {
-  __shared__ int32_t unit_order[kPlanMaxUnits];
+                                                   int H, int n, int32_t* __restrict__ order) {
+  __shared__ int32_t cost[kPlanMaxUnits];
+  __shared__ int32_t by_cost[kPlanMaxUnits];
+  __shared__ uint8_t xcd_of[kPlanMaxUnits];
   const int U = B * H;
   const int tid = threadIdx.x;
+  if (U > kPlanMaxUnits) {
+    for (int u = tid; u < U; u += 256) order[u] = u;
+    return;
+  }
   for (int u = tid; u < U; u += 256) {
     const int b = u / H, h = u % H;
     const int64_t r0 = ((int64_t)(mask_batch > 1 ? b : 0) * H + h) * n;
-    unit_cost[u] = row_ptr[r0 + n] - row_ptr[r0] + n;
+    cost[u] = row_ptr[r0 + n] - row_ptr[r0] + n;
   }
   __syncthreads();
-  if (tid == 0 && U <= kPlanMaxUnits) {
-    // unit ids by (cost desc, id asc): insertion sort
-    for (int u = 0; u < U; ++u) {
-      const int32_t cu = unit_cost[u];
-      int p = u;
-      while (p > 0) {
-        const int prev = unit_order[p - 1];
-        const int32_t cp = unit_cost[prev];
-        if (cp > cu || (cp == cu && prev < u)) break;
-        unit_order[p] = prev;
-        --p;
-      }
-      unit_order[p] = u;
+  for (int u = tid; u < U; u += 256) {
+    const int32_t cu = cost[u];
+    int rank = 0;
+    for (int v = 0; v < U; ++v) {
+      const int32_t cv = cost[v];
+      rank += (cv > cu || (cv == cu && v < u)) ? 1 : 0;
     }
+    by_cost[rank] = u;
+  }
+  __syncthreads();
+  if (tid == 0) {
     int64_t load[kNumXcd];
     int used[kNumXcd], cap[kNumXcd];
     for (int x = 0; x < kNumXcd; ++x) {
@@ -350,25 +533,27 @@ __global__ __launch_bounds__(256) void plan_kernel(const int32_t* __restrict__ r
       used[x] = 0;
       cap[x] = U / kNumXcd + (x < U % kNumXcd ? 1 : 0);
     }
-    // the assignment overwrites unit_cost (each cost is read before)
     for (int p = 0; p < U; ++p) {
-      const int u = unit_order[p];
+      const int u = by_cost[p];
       int best = -1;
       for (int x = 0; x < kNumXcd; ++x) {
         if (used[x] >= cap[x]) continue;
         if (best < 0 || load[x] < load[best]) best = x;
       }
-      load[best] += unit_cost[u];
+      load[best] += cost[u];
       used[best] += 1;
-      unit_cost[u] = -1 - best;
+      xcd_of[u] = (uint8_t)best;
     }
-    int p = 0;
-    for (int x = 0; x < kNumXcd; ++x)
-      for (int u = 0; u < U; ++u)
-        if (unit_cost[u] == -1 - x) unit_order[p++] = u;
+    int start[kNumXcd];
+    int run = 0;
+    for (int x = 0; x < kNumXcd; ++x) {
+      start[x] = run;
+      run += cap[x];
+    }
+    for (int u = 0; u < U; ++u) by_cost[start[xcd_of[u]]++] = u;
   }
   __syncthreads();
-  for (int u = tid; u < U; u += 256) order[u] = U > kPlanMaxUnits ? u : unit_order[u];
+  for (int u = tid; u < U; u += 256) order[u] = by_cost[u];
 }
 
 // ---------------------------------------------------------------------------
@@ -427,13 +612,9 @@ hipError_t launch_score_select(const double* qbar, const double* kbar, int B, in
                      block_scores);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  int N = 1;
-  while (N < n) N <<= 1;
-  if (N < 64) N = 64;
-  const size_t shmem = (size_t)N * sizeof(double) + (size_t)N * sizeof(int) + kSelThreads * sizeof(double) +
-                       4 * sizeof(double) + (size_t)(N / 32) * sizeof(uint32_t);
   const int64_t rows = (int64_t)B * H * n;
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)rows), dim3(kSelThreads), shmem, st, scores, n, N, top_p, k_min,
+  const size_t shmem = 2 * (size_t)n * sizeof(uint64_t);
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)rows), dim3(kSelThreads), shmem, st, scores, n, top_p, k_min,
                      counts, bitmap, words);
   return hipGetLastError();
 }
@@ -450,9 +631,9 @@ hipError_t launch_compact(const uint32_t* bitmap, int words, const int32_t* row_
   return hipGetLastError();
 }
 
-hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n, int32_t* unit_cost_ws,
-                       int32_t* order, hipStream_t st) {
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(256), 0, st, row_ptr, mask_batch, B, H, n, unit_cost_ws, order);
+hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n, int32_t* order,
+                       hipStream_t st) {
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(256), 0, st, row_ptr, mask_batch, B, H, n, order);
   return hipGetLastError();
 }
 

@@ -126,6 +126,47 @@ def test_builder_single_block_and_tiny_sequences():
         assert rep.ok, (S, rep.failing[:3])
 
 
+@pytest.mark.parametrize("top_p,mk", [(0.5, 0.0), (0.3, 0.4), (0.0, 0.25), (0.97, 0.0)])
+def test_builder_exact_ties(top_p, mk):
+    """Bit-identical block scores: constant Q/K (every score of a row equal)
+    and K whose blocks repeat with period 4 (four-way ties per row).  Equal
+    scores are kept lowest index first."""
+    sm = 1.0 / math.sqrt(128)
+    S, H = 64 * 20, 2
+    const = torch.full((1, S, H, 128), 0.25, dtype=torch.bfloat16)
+    gen = torch.Generator().manual_seed(3)
+    q = (torch.randn(1, S, H, 128, generator=gen) * 0.5).to(torch.bfloat16)
+    base = (torch.randn(1, 4 * 64, H, 128, generator=gen) * 0.5).to(torch.bfloat16)
+    k_rep = base.repeat(1, S // (4 * 64), 1, 1).contiguous()
+    for qq, kk in ((const, const), (q, k_rep)):
+        m = ops.build_block_mask(qq.cuda(), kk.cuda(), top_p, mk, sm_scale=sm)
+        rp, ci = m.to_host()
+        o = om.build_block_mask(np64(qq), np64(kk), sm, top_p, mk)
+        rep = compare_masks(rp, ci, o, range(m.rows), top_p, mk)
+        assert rep.ok, rep.failing[:3]
+    # constant rows keep a prefix of indices: k = 10 of 20 in exact arithmetic
+    # (the float64 running sum of ten 1/20 lands one ulp below 0.5, hence 11
+    # is accepted too; the comparator above excuses that boundary)
+    m = ops.build_block_mask(const.cuda(), const.cuda(), 0.5, 0.0, sm_scale=sm)
+    rp, ci = m.to_host()
+    for r in range(m.rows):
+        row = ci[rp[r]:rp[r + 1]]
+        assert len(row) in (10, 11) and np.array_equal(row, np.arange(len(row)))
+
+
+def test_builder_largest_supported_row():
+    """n = 4096 blocks (the largest row): every row against the oracle."""
+    sm = 1.0 / math.sqrt(128)
+    S = 64 * 4096 - 7
+    q, k = positional_qk(1, S, 1, torch.bfloat16, 21)
+    for top_p, mk in ((0.4, 0.01), (0.0, 0.1)):
+        m = ops.build_block_mask(q.cuda(), k.cuda(), top_p, mk, sm_scale=sm)
+        rp, ci = m.to_host()
+        o = om.build_block_mask(np64(q), np64(k), sm, top_p, mk)
+        rep = compare_masks(rp, ci, o, range(m.rows), top_p, mk)
+        assert rep.ok, rep.failing[:3]
+
+
 # --------------------------------------------------------------------------- attention
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
 def test_attention_peaked_logits(dtype):
@@ -213,6 +254,40 @@ def test_attention_strided_views_and_determinism():
     O, _ = oa.attention(np64(q.cpu()), np64(k.cpu()), np64(v.cpu()), rp, ci,
                         1.0 / math.sqrt(128), 1)
     assert within_rounding(np64(o1), O, torch.bfloat16)
+
+
+def greedy_plan(rp, B, H, n, mask_batch, xcds=8):
+    """The plan rule restated in plain Python: unit cost = listed blocks +
+    q-blocks; heaviest first (ties by id) to the least-loaded XCD with room
+    (lowest XCD id on equal load); units listed XCD by XCD, ascending id."""
+    U = B * H
+    cost = []
+    for u in range(U):
+        b, h = divmod(u, H)
+        r0 = ((b if mask_batch > 1 else 0) * H + h) * n
+        cost.append(int(rp[r0 + n] - rp[r0]) + n)
+    cap = [U // xcds + (1 if x < U % xcds else 0) for x in range(xcds)]
+    load, used, where = [0] * xcds, [0] * xcds, [0] * U
+    for u in sorted(range(U), key=lambda u: (-cost[u], u)):
+        best = min((x for x in range(xcds) if used[x] < cap[x]), key=lambda x: (load[x], x))
+        load[best] += cost[u]
+        used[best] += 1
+        where[u] = best
+    return [u for x in range(xcds) for u in range(U) if where[u] == x]
+
+
+@pytest.mark.parametrize("B,H,mask_batch", [(1, 24, 1), (4, 40, 1), (3, 7, 3), (1, 1, 1), (2, 600, 2)])
+def test_plan_follows_greedy_rule(B, H, mask_batch):
+    n = 9
+    rng = np.random.Generator(np.random.PCG64(B * 1000 + H))
+    rows = mask_batch * H * n
+    counts = rng.integers(1, n + 1, size=rows)
+    rp = np.zeros(rows + 1, np.int64)
+    np.cumsum(counts, out=rp[1:])
+    ci = np.concatenate([np.sort(rng.choice(n, c, replace=False)) for c in counts])
+    mask = ops.BlockMask.from_host(rp, ci, mask_batch, H, n)
+    order = ops.plan_block_mask(mask, B, 64 * n).cpu().tolist()
+    assert order == greedy_plan(rp, B, H, n, mask_batch)
 
 
 def test_attention_fp8_small_full():
