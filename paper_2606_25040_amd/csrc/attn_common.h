@@ -18,6 +18,15 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef i16x4 __attribute__((address_space(3))) lds_i16x4;
 typedef i32x2 __attribute__((address_space(3))) lds_i32x2;
 
+// Read-only data seen through the constant address space: the compiler reads
+// it with scalar loads (counted by lgkmcnt), which do not wait behind the tile
+// loads still in flight (vmcnt).  Used for the kv lists and the fp8 block
+// scales, which no kernel writes while attention runs.
+typedef const __attribute__((address_space(4))) int32_t ConstI32;
+typedef const __attribute__((address_space(4))) float ConstF32;
+__device__ inline ConstI32* as_constant(const int32_t* p) { return (ConstI32*)p; }
+__device__ inline ConstF32* as_constant(const float* p) { return (ConstF32*)p; }
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -33,8 +42,9 @@ __device__ inline float pair_sum(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Work item of dispatch slot p.  Items are pairs of neighbouring q-blocks,
-// `np` per (request, head) unit, numbered unit * np + pair.  Slots are dealt
+// Work item of dispatch slot p.  Items are runs of neighbouring q-blocks
+// (one q-block, or a pair), `np` per (request, head) unit, numbered
+// unit * np + index.  Slots are dealt
 // round-robin to the 8 XCDs, so slot p runs on XCD p % 8; XCD x walks item
 // positions [x * chunk, (x + 1) * chunk) of the unit order (the planned
 // order of (request, head) units, or the natural one).  Returns -1 for idle
@@ -65,11 +75,11 @@ __device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
 // Walk of one q-block's kv list (ascending ids, ids outside [0, n) skipped).
 // All lanes hold the same state.
 struct RowWalk {
-  const int32_t* col;
+  ConstI32* col;
   int p, e, n;
   bool dense;
   __device__ void init(const AttnArgs& a, bool is_dense, int b, int h, int i) {
-    col = a.col_idx;
+    col = as_constant(a.col_idx);
     n = a.n;
     dense = is_dense;
     if (dense) {
@@ -95,11 +105,11 @@ struct RowWalk {
 // ascending kv id, skipping ids outside [0, n).  All lanes hold the same
 // state (it lives in scalar registers).
 struct PairWalk {
-  const int32_t* col;
+  ConstI32* col;
   int pa, a1, pb, b1, n;
   bool dense;
   __device__ void init(const AttnArgs& a, bool is_dense, int b, int h, int ip) {
-    col = a.col_idx;
+    col = as_constant(a.col_idx);
     n = a.n;
     dense = is_dense;
     const int ia = 2 * ip, ib = 2 * ip + 1;

@@ -131,7 +131,8 @@ void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
     kb0 = a.row_ptr[mrow];
     kb1 = a.row_ptr[mrow + 1];
   }
-  auto kv_block = [&](int jj) { return DENSE ? jj : a.col_idx[jj]; };
+  ConstI32* cidx = as_constant(a.col_idx);   // scalar loads
+  auto kv_block = [&](int jj) { return DENSE ? jj : cidx[jj]; };
   // ids outside [0, n) are skipped (the builder never emits them)
   auto next_valid = [&](int jj) {
     while (jj < kb1) {

@@ -79,9 +79,9 @@ void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
   const int sel = wave >> 1;
   const int i = 2 * ip + sel;
   const bool q_active = i < n;
-  const float* qsc = a.q_scale + (int64_t)bh * n;
-  const float* ksc = a.k_scale + (int64_t)bh * n;
-  const float* vsc = a.v_scale + (int64_t)bh * n;
+  ConstF32* qsc = as_constant(a.q_scale) + (int64_t)bh * n;   // scalar loads
+  ConstF32* ksc = as_constant(a.k_scale) + (int64_t)bh * n;
+  ConstF32* vsc = as_constant(a.v_scale) + (int64_t)bh * n;
 
   PairWalk walk;
   walk.init(a, DENSE, b, h, ip);
