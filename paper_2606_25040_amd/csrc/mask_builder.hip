@@ -425,6 +425,232 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const double* __res
   if (tid == 0) counts[row] = (int32_t)k;
 }
 
+// Same selection with one wave per row for rows of at most 64 * kWaveMaxPer
+// blocks: lane l keeps the keys and masses of blocks l + 64 e in registers,
+// reductions are wave shuffles, the per-digit histogram lives in the wave's
+// own LDS slice, and the kept set is written as ballots (block 64 e + l is
+// bit l of word pair 2e, 2e + 1).  No workgroup barrier is needed; four rows
+// share a workgroup.
+// ---------------------------------------------------------------------------
+constexpr int kWaveMaxPer = 32;   // n <= 2048
+
+// LDS accesses of one wave take effect in program order; this keeps the
+// compiler from moving them across the point.
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <typename T>
+__device__ inline T wave_bcast(T v, int src) {
+  return __shfl(v, src);
+}
+
+template <int PER>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ? 4 : 2))) void select_wave_kernel(const double* __restrict__ scores, int n, int64_t rows,
+                                                          double top_p, int k_min, int32_t* __restrict__ counts,
+                                                          uint32_t* __restrict__ bitmap, int words) {
+  __shared__ uint32_t hist_cnt_all[4][256];
+  __shared__ uint64_t hist_mass_all[4][256];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= rows) return;
+  uint32_t* hist_cnt = hist_cnt_all[wave];
+  uint64_t* hist_mass = hist_mass_all[wave];
+  const double* s = scores + row * n;
+
+  uint64_t key[PER], mass[PER];
+  double m = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    const double v = j < n ? s[j] : -INFINITY;
+    key[e] = (uint64_t)__double_as_longlong(v);
+    m = fmax(m, v);
+  }
+  for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+  double z = 0.0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    const double x = j < n ? exp(__longlong_as_double((long long)key[e]) - m) : 0.0;
+    mass[e] = (uint64_t)__double_as_longlong(x);
+    z += x;
+  }
+  for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o);
+  uint64_t total = 0, kmin = ~0ull, kmax = 0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    if (j < n) {
+      mass[e] = __double2ull_rn(__longlong_as_double((long long)mass[e]) / z * kMassOne);
+      key[e] = order_key(__longlong_as_double((long long)key[e]));
+      kmin = key[e] < kmin ? key[e] : kmin;
+      kmax = key[e] > kmax ? key[e] : kmax;
+    } else {
+      mass[e] = 0;
+      key[e] = 0;
+    }
+    total += mass[e];
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    total += __shfl_xor(total, o);
+    const uint64_t a = __shfl_xor(kmin, o), b = __shfl_xor(kmax, o);
+    kmin = a < kmin ? a : kmin;
+    kmax = b > kmax ? b : kmax;
+  }
+
+  SelCond cond;
+  cond.any_mass = !(top_p > 0.0);
+  cond.target = cond.any_mass ? 0 : (uint64_t)ceil(fmin(top_p, 1.0) * kMassOne);
+  cond.kk = (uint32_t)(k_min > 1 ? k_min : 1);
+  const bool keep_all = top_p >= 1.0 || cond.kk >= (uint32_t)n || !cond((uint32_t)n, total);
+
+  uint64_t kb = 0;   // keep blocks with key > kb, and key == kb with index <= jb
+  int jb = n;
+  uint32_t k = (uint32_t)n;
+  if (!keep_all) {
+    const uint64_t diff = kmin ^ kmax;
+    int lo = diff ? 64 - __clzll((long long)diff) : 0;
+    uint64_t prefix = lo == 64 ? 0 : (kmin >> lo) << lo;
+    uint64_t mass_above = 0;
+    uint32_t cnt_above = 0, bin_cnt = (uint32_t)n;
+    while (lo > 0) {
+      const int shift = lo > 8 ? lo - 8 : 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        hist_cnt[4 * lane + q] = 0u;
+        hist_mass[4 * lane + q] = 0ull;
+      }
+      wave_lds_sync();
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int j = lane + 64 * e;
+        if (j < n && (lo == 64 || ((key[e] ^ prefix) >> lo) == 0)) {
+          const int bin = (int)((key[e] >> shift) & 255);
+          atomicAdd(&hist_cnt[bin], 1u);
+          atomicAdd((unsigned long long*)&hist_mass[bin], (unsigned long long)mass[e]);
+        }
+      }
+      wave_lds_sync();
+      uint32_t c[4], c4 = 0;
+      uint64_t ms[4], m4 = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        c[q] = hist_cnt[4 * lane + q];
+        ms[q] = hist_mass[4 * lane + q];
+        c4 += c[q];
+        m4 += ms[q];
+      }
+      wave_lds_sync();
+      uint32_t cs = c4;
+      uint64_t msum = m4;
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t vc = __shfl_down(cs, o);
+        const uint64_t vm = __shfl_down(msum, o);
+        if (lane + o < 64) {
+          cs += vc;
+          msum += vm;
+        }
+      }
+      uint32_t cc = cnt_above + (cs - c4);
+      uint64_t mm = mass_above + (msum - m4);
+      bool before = cond(cc, mm);
+      int f_bin = -1;
+      uint32_t f_cnt_above = 0, f_bin_cnt = 0;
+      uint64_t f_mass_above = 0;
+#pragma unroll
+      for (int q = 3; q >= 0; --q) {
+        const uint32_t c2 = cc + c[q];
+        const uint64_t m2 = mm + ms[q];
+        const bool now = cond(c2, m2);
+        if (now && !before) {
+          f_bin = 4 * lane + q;
+          f_cnt_above = cc;
+          f_mass_above = mm;
+          f_bin_cnt = c[q];
+        }
+        before = now;
+        cc = c2;
+        mm = m2;
+      }
+      const int src = __ffsll((long long)__builtin_amdgcn_ballot_w64(f_bin >= 0)) - 1;
+      const int bin = wave_bcast(f_bin, src);
+      cnt_above = wave_bcast(f_cnt_above, src);
+      mass_above = wave_bcast(f_mass_above, src);
+      bin_cnt = wave_bcast(f_bin_cnt, src);
+      prefix = (prefix & ~(255ull << shift)) | ((uint64_t)bin << shift);
+      lo = shift;
+      if (bin_cnt == 1) break;
+    }
+    if (bin_cnt == 1) {
+      // the boundary block is the only candidate left
+      uint64_t my_key = 0;
+      int my_j = -1;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int j = lane + 64 * e;
+        if (j < n && (lo == 64 || ((key[e] ^ prefix) >> lo) == 0)) {
+          my_key = key[e];
+          my_j = j;
+        }
+      }
+      const int src = __ffsll((long long)__builtin_amdgcn_ballot_w64(my_j >= 0)) - 1;
+      kb = wave_bcast(my_key, src);
+      jb = wave_bcast(my_j, src);
+      k = cnt_above + 1;
+    } else {
+      // bin_cnt blocks share the score `prefix` (and so one mass): the
+      // boundary is the t-th of them in index order
+      uint64_t my_mass = 0;
+      bool has_tie = false;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int j = lane + 64 * e;
+        if (j < n && key[e] == prefix) {
+          my_mass = mass[e];
+          has_tie = true;
+        }
+      }
+      const int src = __ffsll((long long)__builtin_amdgcn_ballot_w64(has_tie)) - 1;
+      const uint64_t tie_mass = wave_bcast(my_mass, src);
+      uint32_t t = 1;
+      if (!cond.any_mass && mass_above < cond.target && tie_mass > 0)
+        t = (uint32_t)((cond.target - mass_above + tie_mass - 1) / tie_mass);
+      if (cond.kk > cnt_above && cond.kk - cnt_above > t) t = cond.kk - cnt_above;
+      if (t > bin_cnt) t = bin_cnt;
+      // tied blocks in index order: ballot e covers blocks 64 e .. 64 e + 63
+      uint32_t before_e = 0;
+      int found = -1;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int j = lane + 64 * e;
+        const uint64_t bm = __builtin_amdgcn_ballot_w64(j < n && key[e] == prefix);
+        const uint32_t c = (uint32_t)__popcll(bm);
+        if (found < 0 && before_e + c >= t) {
+          uint64_t x = bm;
+          for (uint32_t r = t - before_e; r > 1; --r) x &= x - 1;
+          found = 64 * e + (__ffsll((long long)x) - 1);
+        }
+        before_e += c;
+      }
+      kb = prefix;
+      jb = found;
+      k = cnt_above + t;
+    }
+  }
+  uint32_t* dst = bitmap + row * words;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    const bool keep = j < n && (keep_all || key[e] > kb || (key[e] == kb && j <= jb));
+    const uint64_t bm = __builtin_amdgcn_ballot_w64(keep);
+    if (lane < 2 && 2 * e + lane < words) dst[2 * e + lane] = (uint32_t)(bm >> (32 * lane));
+  }
+  if (lane == 0) counts[row] = (int32_t)k;
+}
+
 // ---------------------------------------------------------------------------
 // 3. Exclusive scan of the row counts into row_ptr (one workgroup).
 // ---------------------------------------------------------------------------
@@ -613,9 +839,24 @@ hipError_t launch_score_select(const double* qbar, const double* kbar, int B, in
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t rows = (int64_t)B * H * n;
-  const size_t shmem = 2 * (size_t)n * sizeof(uint64_t);
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)rows), dim3(kSelThreads), shmem, st, scores, n, top_p, k_min,
-                     counts, bitmap, words);
+  const dim3 wave_grid((unsigned)((rows + 3) / 4)), wave_block(256);
+  if (n <= 64 * 8) {
+    hipLaunchKernelGGL(select_wave_kernel<8>, wave_grid, wave_block, 0, st, scores, n, rows, top_p, k_min, counts,
+                       bitmap, words);
+  } else if (n <= 64 * 16) {
+    hipLaunchKernelGGL(select_wave_kernel<16>, wave_grid, wave_block, 0, st, scores, n, rows, top_p, k_min, counts,
+                       bitmap, words);
+  } else if (n <= 64 * 24) {
+    hipLaunchKernelGGL(select_wave_kernel<24>, wave_grid, wave_block, 0, st, scores, n, rows, top_p, k_min, counts,
+                       bitmap, words);
+  } else if (n <= 64 * kWaveMaxPer) {
+    hipLaunchKernelGGL(select_wave_kernel<kWaveMaxPer>, wave_grid, wave_block, 0, st, scores, n, rows, top_p, k_min,
+                       counts, bitmap, words);
+  } else {
+    const size_t shmem = 2 * (size_t)n * sizeof(uint64_t);
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)rows), dim3(kSelThreads), shmem, st, scores, n, top_p, k_min,
+                       counts, bitmap, words);
+  }
   return hipGetLastError();
 }
 

@@ -154,6 +154,21 @@ def test_builder_exact_ties(top_p, mk):
         assert len(row) in (10, 11) and np.array_equal(row, np.arange(len(row)))
 
 
+@pytest.mark.parametrize("n_blocks", [511, 700, 1500, 2000])
+def test_builder_row_lengths_every_selection_path(n_blocks):
+    """Rows of 511, 700, 1500 and 2000 blocks (each register budget of the
+    one-wave-per-row selection), every row against the oracle."""
+    sm = 1.0 / math.sqrt(128)
+    S = 64 * n_blocks - 13
+    q, k = positional_qk(1, S, 1, torch.bfloat16, n_blocks)
+    for top_p, mk in ((0.45, 0.02), (0.0, 0.07), (0.9, 0.0)):
+        m = ops.build_block_mask(q.cuda(), k.cuda(), top_p, mk, sm_scale=sm)
+        rp, ci = m.to_host()
+        o = om.build_block_mask(np64(q), np64(k), sm, top_p, mk)
+        rep = compare_masks(rp, ci, o, range(m.rows), top_p, mk)
+        assert rep.ok, (n_blocks, top_p, mk, rep.failing[:3])
+
+
 def test_builder_largest_supported_row():
     """n = 4096 blocks (the largest row): every row against the oracle."""
     sm = 1.0 / math.sqrt(128)
