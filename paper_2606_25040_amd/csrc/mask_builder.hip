@@ -62,61 +62,68 @@ __global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int 
 
 // ---------------------------------------------------------------------------
 // 2a. Block scores s = sm_scale * qbar kbar^T per (request, head): a float64
-// GEMM tile of 64 x 64 outputs per workgroup, k-dim staged through LDS.
-// Writes float64 scores into the workspace and, optionally, fp32 copies.
+// GEMM tile of 128 x 128 outputs per workgroup of 256 threads (8 x 8 outputs
+// per thread, rows ti + 16 a, columns tj + 16 c), the k-dim staged through
+// LDS in chunks of 16.  Writes float64 scores into the workspace and,
+// optionally, fp32 copies.
 // ---------------------------------------------------------------------------
-constexpr int kST = 64;   // score tile
+constexpr int kST = 128;  // score tile
 constexpr int kSK = 16;   // k-chunk
 
 __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ qbar,
                                                     const double* __restrict__ kbar, int n, double sm_scale,
                                                     double* __restrict__ scores, float* __restrict__ scores32) {
-  __shared__ double qs[kSK][kST + 1];
-  __shared__ double ks[kSK][kST + 1];
+  __shared__ double qs[kSK][kST + 2];
+  __shared__ double ks[kSK][kST + 2];
   const int bh = blockIdx.z;
   const int i0 = blockIdx.y * kST, j0 = blockIdx.x * kST;
   const double* qb = qbar + (int64_t)bh * n * kHeadDim;
   const double* kb = kbar + (int64_t)bh * n * kHeadDim;
   const int tid = threadIdx.x;
-  const int ti = tid / 16, tj = tid % 16;   // 16 x 16 threads, 4 x 4 outputs each
-  double acc[4][4];
+  const int ti = tid / 16, tj = tid % 16;
+  double acc[8][8];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 8; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[a][c] = 0.0;
+    for (int c = 0; c < 8; ++c) acc[a][c] = 0.0;
   for (int kk = 0; kk < kHeadDim; kk += kSK) {
-    for (int e = tid; e < kST * kSK; e += 256) {
-      const int r = e / kSK, d = e % kSK;
-      qs[d][r] = (i0 + r < n) ? qb[(int64_t)(i0 + r) * kHeadDim + kk + d] : 0.0;
-      ks[d][r] = (j0 + r < n) ? kb[(int64_t)(j0 + r) * kHeadDim + kk + d] : 0.0;
+    // 128 rows x 16 dims of each operand: thread -> (row, 8-dim half) pairs
+    for (int e = tid; e < kST * 2; e += 256) {
+      const int r = e >> 1, d0 = (e & 1) * 8;
+      const bool qin = i0 + r < n, kin = j0 + r < n;
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        qs[d0 + d][r] = qin ? qb[(int64_t)(i0 + r) * kHeadDim + kk + d0 + d] : 0.0;
+        ks[d0 + d][r] = kin ? kb[(int64_t)(j0 + r) * kHeadDim + kk + d0 + d] : 0.0;
+      }
     }
     __syncthreads();
-#pragma unroll
+#pragma unroll 4
     for (int d = 0; d < kSK; ++d) {
-      double qa[4], kc[4];
+      double qa[8], kc[8];
 #pragma unroll
-      for (int a = 0; a < 4; ++a) qa[a] = qs[d][ti + 16 * a];
+      for (int a = 0; a < 8; ++a) qa[a] = qs[d][ti + 16 * a];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) kc[c] = ks[d][tj + 16 * c];
+      for (int c = 0; c < 8; ++c) kc[c] = ks[d][tj + 16 * c];
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int a = 0; a < 8; ++a)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[a][c] = fma(qa[a], kc[c], acc[a][c]);
+        for (int c = 0; c < 8; ++c) acc[a][c] = fma(qa[a], kc[c], acc[a][c]);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
+  for (int a = 0; a < 8; ++a) {
     const int i = i0 + ti + 16 * a;
     if (i >= n) continue;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
+    for (int c = 0; c < 8; ++c) {
       const int j = j0 + tj + 16 * c;
       if (j >= n) continue;
-      const double s = sm_scale * acc[a][c];
+      const double v = sm_scale * acc[a][c];
       const int64_t o = ((int64_t)bh * n + i) * n + j;
-      scores[o] = s;
-      if (scores32) scores32[o] = (float)s;
+      scores[o] = v;
+      if (scores32) scores32[o] = (float)v;
     }
   }
 }
@@ -652,30 +659,48 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
 }
 
 // ---------------------------------------------------------------------------
-// 3. Exclusive scan of the row counts into row_ptr (one workgroup).
+// 3. Exclusive scan of the row counts into row_ptr.  Workgroup b scans rows
+// [1024 b, 1024 b + 1024): it first sums every count before its range itself
+// (coalesced reads; the counts are small and L2-resident), then scans its own
+// 1024 counts with wave prefix sums.  No inter-workgroup communication.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ counts, int64_t rows,
-                                                    int32_t* __restrict__ row_ptr) {
-  __shared__ int32_t part[1024];
-  const int tid = threadIdx.x;
-  const int64_t per = (rows + 1023) / 1024;
-  const int64_t r0 = tid * per;
-  int32_t sum = 0;
-  for (int64_t r = r0; r < r0 + per && r < rows; ++r) sum += counts[r];
-  part[tid] = sum;
+constexpr int kScanThreads = 1024;
+
+__device__ inline int32_t wave_incl_scan(int32_t v, int lane) {
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t u = __shfl_up(v, o);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __restrict__ counts, int64_t rows,
+                                                            int32_t* __restrict__ row_ptr) {
+  __shared__ int32_t wsum[kScanThreads / 64];
+  __shared__ int32_t base_s;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * kScanThreads;
+  // sum of all counts before this workgroup's range
+  int32_t before = 0;
+  for (int64_t r = tid; r < r0; r += kScanThreads) before += counts[r];
+  for (int o = 32; o > 0; o >>= 1) before += __shfl_xor(before, o);
+  if (lane == 0) wsum[wave] = before;
   __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int32_t v = tid >= off ? part[tid - off] : 0;
-    __syncthreads();
-    part[tid] += v;
-    __syncthreads();
+  if (tid == 0) {
+    int32_t t = 0;
+    for (int w = 0; w < kScanThreads / 64; ++w) t += wsum[w];
+    base_s = t;
   }
-  int32_t run = tid ? part[tid - 1] : 0;
-  if (tid == 0) row_ptr[0] = 0;
-  for (int64_t r = r0; r < r0 + per && r < rows; ++r) {
-    run += counts[r];
-    row_ptr[r + 1] = run;
-  }
+  __syncthreads();
+  const int64_t r = r0 + tid;
+  const int32_t c = r < rows ? counts[r] : 0;
+  const int32_t incl = wave_incl_scan(c, lane);
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int32_t off = base_s;
+  for (int w = 0; w < wave; ++w) off += wsum[w];
+  if (r < rows) row_ptr[r + 1] = off + incl;
+  if (r == 0) row_ptr[0] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -861,7 +886,8 @@ hipError_t launch_score_select(const double* qbar, const double* kbar, int B, in
 }
 
 hipError_t launch_scan_counts(const int32_t* counts, int64_t rows, int32_t* row_ptr, hipStream_t st) {
-  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, st, counts, rows, row_ptr);
+  const unsigned blocks = (unsigned)((rows + kScanThreads - 1) / kScanThreads);
+  hipLaunchKernelGGL(scan_kernel, dim3(blocks), dim3(kScanThreads), 0, st, counts, rows, row_ptr);
   return hipGetLastError();
 }
 
