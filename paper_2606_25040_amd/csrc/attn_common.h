@@ -72,35 +72,6 @@ __device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
 // Wait until at most n vector-memory loads of this wave are outstanding.
 #define CHORUS_WAIT_VMCNT(n) asm volatile("s_waitcnt vmcnt(" #n ")" ::: "memory")
 
-// Walk of one q-block's kv list (ascending ids, ids outside [0, n) skipped).
-// All lanes hold the same state.
-struct RowWalk {
-  ConstI32* col;
-  int p, e, n;
-  bool dense;
-  __device__ void init(const AttnArgs& a, bool is_dense, int b, int h, int i) {
-    col = as_constant(a.col_idx);
-    n = a.n;
-    dense = is_dense;
-    if (dense) {
-      p = 0;
-      e = n;
-    } else {
-      const int64_t r = ((int64_t)(a.mask_batch > 1 ? b : 0) * a.H + h) * n + i;
-      p = a.row_ptr[r];
-      e = a.row_ptr[r + 1];
-    }
-  }
-  __device__ int next() {
-    while (p < e) {
-      const int j = dense ? p : col[p];
-      ++p;
-      if (j >= 0 && j < n) return j;
-    }
-    return INT32_MAX;
-  }
-};
-
 // Walk of the merged kv lists of the two q-blocks (2p, 2p + 1) of a pair in
 // ascending kv id, skipping ids outside [0, n).  All lanes hold the same
 // state (it lives in scalar registers).
