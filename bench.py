@@ -72,10 +72,11 @@ def traffic_from_profile(kernel_file: str, workload: str, src_hash: str):
 
 
 def cpu_baseline(wl, inp, budget_s: float):
-    """Oracle (plain NumPy float64) on a bounded sample: the mask builder for
-    head 0 of the mask source, then attention of head 0's q-blocks in order
-    until the time budget is spent.  Returns effective TFLOP/s on computed
-    blocks and a description."""
+    """Oracle (plain NumPy float64) on a bounded sample of the same workload:
+    head by head of request 0, the oracle mask builder for the head (or the
+    fixed mask's rows) followed by the oracle attention of that head's
+    q-blocks in order, until about ``budget_s`` seconds of work are spent.
+    Returns effective TFLOP/s on computed blocks and a description."""
     from oracle import attention as oa
     from oracle import mask as om
     try:
@@ -84,39 +85,45 @@ def cpu_baseline(wl, inp, budget_s: float):
     except Exception:  # noqa: BLE001
         threads = 1
     cores = len(os.sched_getaffinity(0))
-    t0 = time.perf_counter()
-    mq = inp.mask_q[0, :, 0].float().numpy() if inp.mask_q is not None else None
-    mk = inp.mask_k[0, :, 0].float().numpy() if inp.mask_k is not None else None
-    if mq is not None:
-        s = om.block_scores(om.pool_means(mq), om.pool_means(mk), wl.sm_scale)
-        rows = [om.select_row(s[i], wl.top_p, wl.min_top_k) for i in range(wl.n_blocks)]
-    else:
-        rp, ci = inp.random_mask
-        rows = [ci[rp[i]:rp[i + 1]] for i in range(wl.n_blocks)]
-    t_build = time.perf_counter() - t0
-    if wl.dtype == "fp8":
-        from oracle import fp8 as of
-        qh, kh, vh = (of.dequantize_blockwise(*of.quantize_blockwise(x[:1, :, :1].float().numpy()))
-                      [0, :, 0] for x in (inp.q, inp.k, inp.v))
-    else:
-        qh, kh, vh = (x[0, :, 0].float().numpy() for x in (inp.q, inp.k, inp.v))
+    t_build = t_attn = 0.0
     pairs = 0
-    done = 0
-    t1 = time.perf_counter()
-    for i in range(wl.n_blocks):
-        oa.attention_block(qh, kh, vh, rows[i], i, wl.sm_scale)
-        pairs += len(rows[i])
-        done += 1
-        if time.perf_counter() - t1 > budget_s:
+    blocks_done = 0
+    heads_done = 0
+    for h in range(wl.H):
+        t0 = time.perf_counter()
+        if inp.mask_q is not None:
+            mq = inp.mask_q[0, :, h].float().numpy()
+            mk = inp.mask_k[0, :, h].float().numpy()
+            s = om.block_scores(om.pool_means(mq), om.pool_means(mk), wl.sm_scale)
+            rows = [om.select_row(s[i], wl.top_p, wl.min_top_k) for i in range(wl.n_blocks)]
+        else:
+            rp, ci = inp.random_mask
+            base = h * wl.n_blocks
+            rows = [ci[rp[base + i]:rp[base + i + 1]] for i in range(wl.n_blocks)]
+        if wl.dtype == "fp8":
+            from oracle import fp8 as of
+            qh, kh, vh = (of.dequantize_blockwise(*of.quantize_blockwise(x[:1, :, h:h + 1].float().numpy()))
+                          [0, :, 0] for x in (inp.q, inp.k, inp.v))
+        else:
+            qh, kh, vh = (x[0, :, h].float().numpy() for x in (inp.q, inp.k, inp.v))
+        t1 = time.perf_counter()
+        t_build += t1 - t0
+        done = 0
+        for i in range(wl.n_blocks):
+            oa.attention_block(qh, kh, vh, rows[i], i, wl.sm_scale)
+            pairs += len(rows[i])
+            done += 1
+            if t_build + t_attn + (time.perf_counter() - t1) > budget_s:
+                break
+        t_attn += time.perf_counter() - t1
+        blocks_done += done
+        heads_done += 1
+        if t_build + t_attn > budget_s:
             break
-    t_attn = time.perf_counter() - t1
-    # builder share for the q-blocks covered (one head's builder serves n q-blocks)
-    t = t_attn + t_build * done / wl.n_blocks
-    value = pairs * FLOP_PER_PAIR / t / 1e12
-    sample = (f"oracle mask builder for head 0 ({wl.n_blocks} rows, {t_build:.2f} s) + oracle "
-              f"attention (gather form, float64) for q-blocks 0..{done - 1} of head 0 of request 0 "
-              f"({pairs} computed block pairs, {t_attn:.2f} s); builder time pro-rated to those "
-              f"q-blocks; float64 NumPy, BLAS threads {threads}")
+    value = pairs * FLOP_PER_PAIR / (t_build + t_attn) / 1e12
+    sample = (f"request 0, heads 0..{heads_done - 1}: oracle mask builder per head ({t_build:.2f} s incl. "
+              f"input casts) + oracle attention (gather form, float64) of {blocks_done} q-blocks in order "
+              f"({pairs} computed block pairs, {t_attn:.2f} s); float64 NumPy, BLAS threads {threads}")
     return {"value": value, "unit": "TFLOP/s", "cores": min(threads, cores), "kind": "oracle",
             "sample": sample}
 
