@@ -17,6 +17,10 @@ Generation"):
   Retrieval" and "Minimum top-k guarantee"; knobs in Sec. 4.1).
 * ``fp8``        -- OCP e4m3fn round-to-nearest-even codec and the per-(head,
   64-token block) quantiser feeding the FP8 path (Sec. 3.2, FP8 backend).
+* ``mass``       -- the true block attention mass of a request, the top-p /
+  top-k mask selected from it (the masks a historical request records, Sec.
+  3.2 "Mask Caching and Retrieval") and the coverage of a mask on a request
+  (Sec. 3.2, Obs. 1).
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute force,
 closed forms, library routines and invariants.  The one part with no outside
@@ -25,4 +29,4 @@ output or worked example for this path ("parity unpinned" against the paper
 itself; pinned against the mathematics).
 """
 
-from . import attention, fp8, mask  # noqa: F401
+from . import attention, fp8, mask, mass  # noqa: F401
