@@ -246,6 +246,69 @@ chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const 
                                                void* workspace, size_t workspace_bytes,
                                                void* stream);
 
+/* ---------------------------------------------------------------------------
+ * True block attention mass -- Sec. 3.2 "Mask Caching and Retrieval": a
+ * historical request runs its own attention anyway, and the mask stored for
+ * reuse is selected from that attention map by top-p with a top-k floor; Sec.
+ * 3.2 Obs. 1 judges a mask by the share of the attention mass it covers.
+ *
+ * For every request b, head h, q-block i and kv-block j:
+ *   mass[b,h,i,j] = (1 / |T_i|) * sum_{r in T_i} sum_{c in T_j}
+ *                   exp(sm_scale <Q[b,r,h,:], K[b,c,h,:]> - lse[b,h,r])
+ * where T_i are the valid tokens of block i and lse is the log-sum-exp of the
+ * DENSE attention of the same q and k with the same sm_scale (as written by
+ * chorus_block_sparse_attn_fwd with mask = NULL).  Each row mass[b,h,i,:] is
+ * then the mean attention distribution of q-block i over kv blocks (sums to
+ * 1 up to rounding).  The scores are recomputed with fp32 accumulation.
+ *
+ * q, k  : [B, S, H, D] f16 or bf16 (dtype), read only.
+ * lse   : device float32 [B, H, S], read only.
+ * mass  : out, device float32 [B, H, n_blocks, n_blocks], row-major.
+ * ------------------------------------------------------------------------- */
+chorus_status chorus_attn_block_mass(chorus_dtype dtype, const chorus_shape* shape,
+                                     const chorus_tensor* q, const chorus_tensor* k, const float* lse,
+                                     float sm_scale, float* mass, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Block mask from block masses (the selection of Sec. 3.2 "Mask Caching and
+ * Retrieval" applied to an attention map): for every row mass[b,h,i,:]
+ * (non-negative), blocks are ranked by (mass descending, j ascending) and the
+ * first min(n, max(k_p, k_min, 1)) are kept, where k_p is the smallest k >= 1
+ * whose share of the row's total mass is >= top_p (0 if top_p <= 0, n if
+ * top_p >= 1) and k_min = ceil(min_top_k * n - 1e-9).  A row with zero total
+ * mass never reaches a top_p > 0, so it keeps every block (with top_p = 0 the
+ * floor alone decides).  Output as chorus_build_block_mask (mask_batch = B).
+ *
+ * mass          : device float32 [B, H, n_blocks, n_blocks], read only.
+ * row_ptr       : out, device int32 [B * H * n_blocks + 1].
+ * col_idx       : out, device int32 [col_capacity], col_capacity >=
+ *                 B * H * n_blocks^2 (else CHORUS_ERR_CAPACITY).
+ * workspace     : device scratch of chorus_select_block_mask_workspace_size()
+ *                 bytes, 256-byte aligned.
+ * Supports n_blocks <= 4096.
+ * ------------------------------------------------------------------------- */
+size_t chorus_select_block_mask_workspace_size(const chorus_shape* shape);
+chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* mass, double top_p,
+                                       double min_top_k, int32_t* row_ptr, int32_t* col_idx,
+                                       int64_t col_capacity, void* workspace, size_t workspace_bytes,
+                                       void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Coverage of a mask (Sec. 3.2 Obs. 1): the share of the requests' attention
+ * mass that falls inside the blocks the mask keeps, every valid query
+ * weighted equally:
+ *   coverage[b,h] = (1 / S) * sum_i |T_i| * sum_{j in row m} mass[b,h,i,j]
+ * with m = ((mask_batch > 1 ? b : 0) * H + h) * n_blocks + i and mass as
+ * written by chorus_attn_block_mass for those requests.  Ids outside
+ * [0, n_blocks) are ignored.
+ *
+ * mask     : the mask to judge (mask_batch 1 or B).
+ * mass     : device float32 [B, H, n_blocks, n_blocks], read only.
+ * coverage : out, device float64 [B, H].
+ * ------------------------------------------------------------------------- */
+chorus_status chorus_mask_coverage(const chorus_shape* shape, const chorus_block_mask* mask,
+                                   const float* mass, double* coverage, void* stream);
+
 /* Human-readable name of a status, and the detail of the calling thread's
  * last error (empty string if none).  Both return static / thread-local
  * storage owned by the library. */

@@ -8,13 +8,16 @@ and fails loudly if it has not been built.
 
 from .ops import (  # noqa: F401
     BlockMask,
+    attn_block_mass,
     block_sparse_attn_fwd,
     block_sparse_attn_fwd_bf16,
     block_sparse_attn_fwd_f16,
     block_sparse_attn_fwd_fp8,
     build_block_mask,
     load_library,
+    mask_coverage,
     plan_block_mask,
     quantize_fp8_blockwise,
+    select_block_mask,
     validate_block_mask,
 )

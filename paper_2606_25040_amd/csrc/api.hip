@@ -60,6 +60,12 @@ static chorus_status check_tensor(const chorus_tensor* t, const char* name, size
 
 static TensorArg targ(const chorus_tensor* t) { return {t->data, t->stride_b, t->stride_s, t->stride_h}; }
 
+// Tile loads address a token row of one (request, head) with a 32-bit byte
+// offset from the head's base: (S - 1) * stride_s * element size + 256 must fit.
+static bool offsets_fit(int32_t S, int64_t stride_s, size_t es) {
+  return (int64_t)(S - 1) * stride_s * (int64_t)es + 256 <= (int64_t)UINT32_MAX;
+}
+
 static chorus_status check_mask(const chorus_shape* s, const chorus_block_mask* m) {
   if (!m) return fail(CHORUS_ERR_INVALID_ARG, "mask is NULL");
   if (m->block != kBlock) return fail(CHORUS_ERR_UNSUPPORTED, "mask block %d unsupported (only 64)", m->block);
@@ -252,7 +258,7 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   const int n = blocks_of(shape->S);
   const int64_t items = (int64_t)shape->B * shape->H * n;
   if (items > INT32_MAX) return fail(CHORUS_ERR_UNSUPPORTED, "too many work items");
-  if ((int64_t)(n - 1) * kBlock * std::max(std::max(q->stride_s, k->stride_s), v->stride_s) * 2 > UINT32_MAX)
+  if (!offsets_fit(shape->S, std::max(std::max(q->stride_s, k->stride_s), v->stride_s), es))
     return fail(CHORUS_ERR_UNSUPPORTED, "token stride too large for 32-bit in-head offsets");
   if (schedule) {
     if (!schedule->order) return fail(CHORUS_ERR_INVALID_ARG, "schedule order is NULL");
@@ -314,6 +320,84 @@ chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const 
                                                size_t workspace_bytes, void* stream) {
   return chorus_block_sparse_attn_fwd(CHORUS_FP8_E4M3, shape, q, k, v, q_scale, k_scale, v_scale, mask,
                                       schedule, sm_scale, out, lse, workspace, workspace_bytes, stream);
+}
+
+chorus_status chorus_attn_block_mass(chorus_dtype dtype, const chorus_shape* shape,
+                                     const chorus_tensor* q, const chorus_tensor* k, const float* lse,
+                                     float sm_scale, float* mass, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if (dtype != CHORUS_F16 && dtype != CHORUS_BF16)
+    return fail(CHORUS_ERR_UNSUPPORTED, "block mass dtype %d unsupported (f16/bf16)", (int)dtype);
+  if ((st = check_tensor(q, "q", 2))) return st;
+  if ((st = check_tensor(k, "k", 2))) return st;
+  if (!lse || !mass) return fail(CHORUS_ERR_INVALID_ARG, "lse/mass is NULL");
+  if (!std::isfinite(sm_scale) || !(sm_scale > 0.f))
+    return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite and > 0");
+  if (!offsets_fit(shape->S, k->stride_s, 2))
+    return fail(CHORUS_ERR_UNSUPPORTED, "token stride too large for 32-bit in-head offsets");
+  if (shape->H > 65535 || shape->B > 65535) return fail(CHORUS_ERR_UNSUPPORTED, "B or H above 65535");
+  return from_hip(launch_block_mass(dtype, targ(q), targ(k), lse, shape->B, shape->S, shape->H, sm_scale, mass,
+                                    static_cast<hipStream_t>(stream)),
+                  "block_mass");
+}
+
+size_t chorus_select_block_mask_workspace_size(const chorus_shape* shape) {
+  if (!shape || shape->B < 1 || shape->H < 1 || shape->S < 1) return 0;
+  const int n = blocks_of(shape->S);
+  const size_t rows = (size_t)shape->B * shape->H * n;
+  Carver c(nullptr);
+  c.take<int32_t>(rows);
+  c.take<uint32_t>(rows * ((n + 31) / 32));
+  return align_up(c.used, 256);
+}
+
+chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* mass, double top_p,
+                                       double min_top_k, int32_t* row_ptr, int32_t* col_idx,
+                                       int64_t col_capacity, void* workspace, size_t workspace_bytes,
+                                       void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if (!mass) return fail(CHORUS_ERR_INVALID_ARG, "mass is NULL");
+  const int n = blocks_of(shape->S);
+  if (n > kMaxBuilderBlocks)
+    return fail(CHORUS_ERR_UNSUPPORTED, "n_blocks=%d exceeds selection limit %d", n, kMaxBuilderBlocks);
+  if (!(top_p >= 0.0 && top_p <= 1.0)) return fail(CHORUS_ERR_INVALID_ARG, "top_p must be in [0, 1]");
+  if (!(min_top_k >= 0.0 && min_top_k <= 1.0))
+    return fail(CHORUS_ERR_INVALID_ARG, "min_top_k must be in [0, 1]");
+  if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
+  const int64_t rows = (int64_t)shape->B * shape->H * n;
+  if (rows * n > INT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "B*H*n_blocks^2 = %lld exceeds int32 CSR offsets", (long long)(rows * n));
+  if (col_capacity < rows * n)
+    return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
+                (long long)(rows * n));
+  if ((st = check_workspace(workspace, workspace_bytes, chorus_select_block_mask_workspace_size(shape)))) return st;
+  Carver c(workspace);
+  int32_t* counts = c.take<int32_t>(rows);
+  const int words = (n + 31) / 32;
+  uint32_t* bitmap = c.take<uint32_t>(rows * words);
+  const int k_min = (int)std::ceil(min_top_k * (double)n - 1e-9);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = from_hip(launch_select_from_mass(mass, rows, n, top_p, k_min, counts, bitmap, words, s), "select")))
+    return st;
+  if ((st = from_hip(launch_scan_counts(counts, rows, row_ptr, s), "scan"))) return st;
+  return from_hip(launch_compact(bitmap, words, row_ptr, rows, col_idx, s), "compact");
+}
+
+chorus_status chorus_mask_coverage(const chorus_shape* shape, const chorus_block_mask* mask,
+                                   const float* mass, double* coverage, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if ((st = check_mask(shape, mask))) return st;
+  if (!mass || !coverage) return fail(CHORUS_ERR_INVALID_ARG, "mass/coverage is NULL");
+  if (shape->H > 65535 || shape->B > 65535) return fail(CHORUS_ERR_UNSUPPORTED, "B or H above 65535");
+  return from_hip(launch_coverage(mask->row_ptr, mask->col_idx, mask->mask_batch, mass, shape->B, shape->S,
+                                  shape->H, coverage, static_cast<hipStream_t>(stream)),
+                  "coverage");
 }
 
 }  // extern "C"

@@ -58,6 +58,8 @@ hipError_t launch_score_select(const double* qbar, const double* kbar, int B, in
                                double sm_scale, double top_p, int k_min, double* scores,
                                int32_t* counts, uint32_t* bitmap, int words, float* block_scores,
                                hipStream_t st);
+hipError_t launch_select_from_mass(const float* mass, int64_t rows, int n, double top_p, int k_min,
+                                   int32_t* counts, uint32_t* bitmap, int words, hipStream_t st);
 hipError_t launch_scan_counts(const int32_t* counts, int64_t rows, int32_t* row_ptr, hipStream_t st);
 hipError_t launch_compact(const uint32_t* bitmap, int words, const int32_t* row_ptr, int64_t rows,
                           int32_t* col_idx, hipStream_t st);
@@ -65,6 +67,12 @@ hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int
                        hipStream_t st);
 hipError_t launch_validate(const int32_t* row_ptr, const int32_t* col_idx, int64_t rows, int n,
                            int64_t capacity, int32_t* flags, hipStream_t st);
+
+// ---- block mass and coverage (block_mass.hip) ----
+hipError_t launch_block_mass(chorus_dtype dt, TensorArg q, TensorArg k, const float* lse, int B, int S, int H,
+                             float sm_scale, float* mass, hipStream_t st);
+hipError_t launch_coverage(const int32_t* row_ptr, const int32_t* col_idx, int mask_batch, const float* mass, int B,
+                           int S, int H, double* coverage, hipStream_t st);
 
 // ---- fp8 quantiser (quant_fp8.hip) ----
 hipError_t launch_quant_fp8(chorus_dtype in_dt, TensorArg x, TensorArg codes, int B, int S, int H,

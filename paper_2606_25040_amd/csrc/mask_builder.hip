@@ -227,7 +227,11 @@ __device__ uint64_t block_reduce_max_u64(uint64_t v, uint64_t* red) {
 }
 
 // Dynamic LDS: key[n] and mass[n] (uint64 each).
-__global__ __launch_bounds__(kSelThreads) void select_kernel(const double* __restrict__ scores, int n,
+// FROM_MASS: the row holds non-negative block masses (fp32) instead of
+// float64 scores; the ranking key is the mass itself and each block's share
+// is mass / row total instead of the softmax of the scores.
+template <bool FROM_MASS>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const void* __restrict__ in, int n,
                                                              double top_p, int k_min,
                                                              int32_t* __restrict__ counts,
                                                              uint32_t* __restrict__ bitmap, int words) {
@@ -245,31 +249,36 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const double* __res
   __shared__ int bound_j;
 
   const int64_t row = blockIdx.x;
-  const double* s = scores + row * n;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  auto value = [&](int j) -> double {
+    return FROM_MASS ? (double)(static_cast<const float*>(in) + row * n)[j]
+                     : (static_cast<const double*>(in) + row * n)[j];
+  };
 
   for (int w = tid; w < words; w += kSelThreads) {
     bits[w] = 0u;
     ties[w] = 0u;
   }
   // scores -> row max -> exp -> row sum -> fixed-point masses and keys
+  // (masses: the values themselves and their row sum)
   double m = -INFINITY;
   for (int j = tid; j < n; j += kSelThreads) {
-    const double v = s[j];
+    const double v = value(j);
     key[j] = order_key(v);
     m = fmax(m, v);
   }
-  m = block_reduce_max(m, red);
+  if (!FROM_MASS) m = block_reduce_max(m, red);
   double z = 0.0;
   for (int j = tid; j < n; j += kSelThreads) {
-    const double x = exp(s[j] - m);
+    const double x = FROM_MASS ? value(j) : exp(value(j) - m);
     mass[j] = (uint64_t)__double_as_longlong(x);
     z += x;
   }
   z = block_reduce_sum(z, red);
   uint64_t total = 0, kmin = ~0ull, kmax = 0;
   for (int j = tid; j < n; j += kSelThreads) {
-    const uint64_t q = __double2ull_rn(__longlong_as_double((long long)mass[j]) / z * kMassOne);
+    const double share = z > 0.0 ? __longlong_as_double((long long)mass[j]) / z : 0.0;
+    const uint64_t q = __double2ull_rn(share * kMassOne);
     mass[j] = q;
     total += q;
     const uint64_t kj = key[j];
@@ -454,8 +463,8 @@ __device__ inline T wave_bcast(T v, int src) {
   return __shfl(v, src);
 }
 
-template <int PER>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ? 4 : 2))) void select_wave_kernel(const double* __restrict__ scores, int n, int64_t rows,
+template <int PER, bool FROM_MASS>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ? 4 : 2))) void select_wave_kernel(const void* __restrict__ in, int n, int64_t rows,
                                                           double top_p, int k_min, int32_t* __restrict__ counts,
                                                           uint32_t* __restrict__ bitmap, int words) {
   __shared__ uint32_t hist_cnt_all[4][256];
@@ -465,23 +474,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
   if (row >= rows) return;
   uint32_t* hist_cnt = hist_cnt_all[wave];
   uint64_t* hist_mass = hist_mass_all[wave];
-  const double* s = scores + row * n;
+  auto value = [&](int j) -> double {
+    return FROM_MASS ? (double)(static_cast<const float*>(in) + row * n)[j]
+                     : (static_cast<const double*>(in) + row * n)[j];
+  };
 
   uint64_t key[PER], mass[PER];
   double m = -INFINITY;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
-    const double v = j < n ? s[j] : -INFINITY;
+    const double v = j < n ? value(j) : -INFINITY;
     key[e] = (uint64_t)__double_as_longlong(v);
     m = fmax(m, v);
   }
-  for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+  if (!FROM_MASS)
+    for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
   double z = 0.0;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
-    const double x = j < n ? exp(__longlong_as_double((long long)key[e]) - m) : 0.0;
+    const double v = __longlong_as_double((long long)key[e]);
+    const double x = j < n ? (FROM_MASS ? v : exp(v - m)) : 0.0;
     mass[e] = (uint64_t)__double_as_longlong(x);
     z += x;
   }
@@ -491,7 +505,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
     if (j < n) {
-      mass[e] = __double2ull_rn(__longlong_as_double((long long)mass[e]) / z * kMassOne);
+      const double share = z > 0.0 ? __longlong_as_double((long long)mass[e]) / z : 0.0;
+      mass[e] = __double2ull_rn(share * kMassOne);
       key[e] = order_key(__longlong_as_double((long long)key[e]));
       kmin = key[e] < kmin ? key[e] : kmin;
       kmax = key[e] > kmax ? key[e] : kmax;
@@ -855,6 +870,32 @@ hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, 
   return hipGetLastError();
 }
 
+namespace {
+template <bool FROM_MASS>
+hipError_t launch_select(const void* in, int64_t rows, int n, double top_p, int k_min, int32_t* counts,
+                         uint32_t* bitmap, int words, hipStream_t st) {
+  const dim3 wave_grid((unsigned)((rows + 3) / 4)), wave_block(256);
+  if (n <= 64 * 8) {
+    hipLaunchKernelGGL((select_wave_kernel<8, FROM_MASS>), wave_grid, wave_block, 0, st, in, n, rows, top_p, k_min,
+                       counts, bitmap, words);
+  } else if (n <= 64 * 16) {
+    hipLaunchKernelGGL((select_wave_kernel<16, FROM_MASS>), wave_grid, wave_block, 0, st, in, n, rows, top_p, k_min,
+                       counts, bitmap, words);
+  } else if (n <= 64 * 24) {
+    hipLaunchKernelGGL((select_wave_kernel<24, FROM_MASS>), wave_grid, wave_block, 0, st, in, n, rows, top_p, k_min,
+                       counts, bitmap, words);
+  } else if (n <= 64 * kWaveMaxPer) {
+    hipLaunchKernelGGL((select_wave_kernel<kWaveMaxPer, FROM_MASS>), wave_grid, wave_block, 0, st, in, n, rows,
+                       top_p, k_min, counts, bitmap, words);
+  } else {
+    const size_t shmem = 2 * (size_t)n * sizeof(uint64_t);
+    hipLaunchKernelGGL((select_kernel<FROM_MASS>), dim3((unsigned)rows), dim3(kSelThreads), shmem, st, in, n, top_p,
+                       k_min, counts, bitmap, words);
+  }
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n, double sm_scale,
                                double top_p, int k_min, double* scores, int32_t* counts, uint32_t* bitmap,
                                int words, float* block_scores, hipStream_t st) {
@@ -863,26 +904,12 @@ hipError_t launch_score_select(const double* qbar, const double* kbar, int B, in
                      block_scores);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t rows = (int64_t)B * H * n;
-  const dim3 wave_grid((unsigned)((rows + 3) / 4)), wave_block(256);
-  if (n <= 64 * 8) {
-    hipLaunchKernelGGL(select_wave_kernel<8>, wave_grid, wave_block, 0, st, scores, n, rows, top_p, k_min, counts,
-                       bitmap, words);
-  } else if (n <= 64 * 16) {
-    hipLaunchKernelGGL(select_wave_kernel<16>, wave_grid, wave_block, 0, st, scores, n, rows, top_p, k_min, counts,
-                       bitmap, words);
-  } else if (n <= 64 * 24) {
-    hipLaunchKernelGGL(select_wave_kernel<24>, wave_grid, wave_block, 0, st, scores, n, rows, top_p, k_min, counts,
-                       bitmap, words);
-  } else if (n <= 64 * kWaveMaxPer) {
-    hipLaunchKernelGGL(select_wave_kernel<kWaveMaxPer>, wave_grid, wave_block, 0, st, scores, n, rows, top_p, k_min,
-                       counts, bitmap, words);
-  } else {
-    const size_t shmem = 2 * (size_t)n * sizeof(uint64_t);
-    hipLaunchKernelGGL(select_kernel, dim3((unsigned)rows), dim3(kSelThreads), shmem, st, scores, n, top_p, k_min,
-                       counts, bitmap, words);
-  }
-  return hipGetLastError();
+  return launch_select<false>(scores, (int64_t)B * H * n, n, top_p, k_min, counts, bitmap, words, st);
+}
+
+hipError_t launch_select_from_mass(const float* mass, int64_t rows, int n, double top_p, int k_min,
+                                   int32_t* counts, uint32_t* bitmap, int words, hipStream_t st) {
+  return launch_select<true>(mass, rows, n, top_p, k_min, counts, bitmap, words, st);
 }
 
 hipError_t launch_scan_counts(const int32_t* counts, int64_t rows, int32_t* row_ptr, hipStream_t st) {

@@ -52,6 +52,8 @@ EXPORTS = [
     "chorus_quantize_fp8_blockwise", "chorus_attn_workspace_size",
     "chorus_block_sparse_attn_fwd", "chorus_block_sparse_attn_fwd_f16",
     "chorus_block_sparse_attn_fwd_bf16", "chorus_block_sparse_attn_fwd_fp8",
+    "chorus_attn_block_mass", "chorus_select_block_mask_workspace_size", "chorus_select_block_mask",
+    "chorus_mask_coverage",
     "chorus_status_string", "chorus_last_error", "chorus_version",
 ]
 
@@ -90,6 +92,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "chorus_block_sparse_attn_fwd_fp8": (I32, [P(Shape), P(Tensor), P(Tensor), P(Tensor), VP,
                                                    VP, VP, P(Mask), P(Schedule), F32, P(Tensor),
                                                    VP, VP, SZ, VP]),
+        "chorus_attn_block_mass": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, F32, VP, VP]),
+        "chorus_select_block_mask_workspace_size": (SZ, [P(Shape)]),
+        "chorus_select_block_mask": (I32, [P(Shape), VP, F64, F64, VP, VP, I64, VP, SZ, VP]),
+        "chorus_mask_coverage": (I32, [P(Shape), P(Mask), VP, VP, VP]),
         "chorus_status_string": (ctypes.c_char_p, [I32]),
         "chorus_last_error": (ctypes.c_char_p, []),
         "chorus_version": (I32, []),
@@ -321,3 +327,62 @@ def block_sparse_attn_fwd_bf16(q, k, v, mask, **kw):
 def block_sparse_attn_fwd_fp8(q, k, v, q_scale, k_scale, v_scale, mask, **kw):
     assert q.dtype == torch.uint8
     return block_sparse_attn_fwd(q, k, v, mask, scales=(q_scale, k_scale, v_scale), **kw)
+
+
+def attn_block_mass(q: torch.Tensor, k: torch.Tensor, lse: torch.Tensor, sm_scale: float | None = None,
+                    out: torch.Tensor | None = None) -> torch.Tensor:
+    """chorus_attn_block_mass: true block attention mass [B, H, n, n] (fp32)
+    of ``q, k [B, S, H, D]`` given the dense attention's ``lse [B, H, S]``."""
+    L = load_library()
+    if q.shape != k.shape or q.dtype != k.dtype:
+        raise ValueError("q and k must share shape and dtype")
+    B, S, H, D = q.shape
+    n = (S + 63) // 64
+    if lse.shape != (B, H, S) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 [B, H, S] tensor")
+    sm = (1.0 / math.sqrt(D)) if sm_scale is None else sm_scale
+    mass = out if out is not None else torch.empty((B, H, n, n), dtype=torch.float32, device=q.device)
+    if mass.shape != (B, H, n, n) or mass.dtype != torch.float32 or not mass.is_contiguous():
+        raise ValueError("out must be a contiguous float32 [B, H, n, n] tensor")
+    st = L.chorus_attn_block_mass(_dtype_code(q), ctypes.byref(_shape(q)), ctypes.byref(_tensor(q)),
+                                  ctypes.byref(_tensor(k)), lse.data_ptr(), sm, mass.data_ptr(), _stream())
+    _check(st, "chorus_attn_block_mass")
+    return mass
+
+
+def select_block_mask(mass: torch.Tensor, S: int, top_p: float, min_top_k: float,
+                      out: BlockMask | None = None, workspace: torch.Tensor | None = None) -> BlockMask:
+    """chorus_select_block_mask: CSR mask (mask_batch = B) cut from block
+    masses ``mass [B, H, n, n]`` of a sequence of S tokens."""
+    L = load_library()
+    B, H, n, n2 = mass.shape
+    if n != n2 or n != (S + 63) // 64 or mass.dtype != torch.float32 or not mass.is_contiguous():
+        raise ValueError("mass must be a contiguous float32 [B, H, n, n] tensor with n = ceil(S / 64)")
+    shape = Shape(B, S, H, 128)
+    rows = B * H * n
+    m = out if out is not None else BlockMask(
+        torch.empty(rows + 1, dtype=torch.int32, device=mass.device),
+        torch.empty(rows * n, dtype=torch.int32, device=mass.device), B, H, n)
+    need = L.chorus_select_block_mask_workspace_size(ctypes.byref(shape))
+    ws = workspace if workspace is not None and workspace.numel() >= need + 256 else \
+        _workspace(need, mass.device)
+    st = L.chorus_select_block_mask(ctypes.byref(shape), mass.data_ptr(), top_p, min_top_k,
+                                    m.row_ptr.data_ptr(), m.col_idx.data_ptr(), m.col_idx.numel(),
+                                    _aligned(ws), need, _stream())
+    _check(st, "chorus_select_block_mask")
+    return m
+
+
+def mask_coverage(mask: BlockMask, mass: torch.Tensor, S: int) -> torch.Tensor:
+    """chorus_mask_coverage: coverage [B, H] (float64) of ``mask`` on the
+    requests whose block masses are ``mass [B, H, n, n]``."""
+    L = load_library()
+    B, H, n, _ = mass.shape
+    if mass.dtype != torch.float32 or not mass.is_contiguous():
+        raise ValueError("mass must be a contiguous float32 tensor")
+    cov = torch.empty((B, H), dtype=torch.float64, device=mass.device)
+    cm = mask.as_c()
+    st = L.chorus_mask_coverage(ctypes.byref(Shape(B, S, H, 128)), ctypes.byref(cm), mass.data_ptr(),
+                                cov.data_ptr(), _stream())
+    _check(st, "chorus_mask_coverage")
+    return cov

@@ -113,3 +113,30 @@ def test_other_entry_points_check_arguments(lib):
     assert lib.chorus_plan_block_mask(ctypes.byref(shp), ctypes.byref(m), None, None, 0, None) == 1
     assert lib.chorus_validate_block_mask(ctypes.byref(m), 10, None, None) == 1
     assert lib.chorus_build_block_mask_workspace_size(ctypes.byref(shape(S=75600, H=40))) > 0
+
+
+def test_block_mass_selection_and_coverage_check_arguments(lib):
+    shp = shape(B=1, S=100, H=2)
+    t = t4()
+    assert lib.chorus_attn_block_mass(ops.FP8_E4M3, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
+                                      FAKE, 0.088, FAKE, None) == 2
+    assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
+                                      None, 0.088, FAKE, None) == 1
+    assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
+                                      FAKE, -1.0, FAKE, None) == 1
+    assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shape(D=64)), ctypes.byref(t), ctypes.byref(t),
+                                      FAKE, 0.088, FAKE, None) == 2
+    need = lib.chorus_select_block_mask_workspace_size(ctypes.byref(shp))
+    assert need > 0
+    sel = lib.chorus_select_block_mask
+    assert sel(ctypes.byref(shp), FAKE, 1.5, 0.0, FAKE, FAKE, 8, FAKE, need, None) == 1
+    assert sel(ctypes.byref(shp), FAKE, 0.5, 0.0, FAKE, FAKE, 7, FAKE, need, None) == 3
+    assert sel(ctypes.byref(shp), FAKE, 0.5, 0.0, FAKE, FAKE, 8, FAKE, 16, None) == 5
+    assert sel(ctypes.byref(shp), None, 0.5, 0.0, FAKE, FAKE, 8, FAKE, need, None) == 1
+    assert sel(ctypes.byref(shape(S=64 * 4097)), FAKE, 0.5, 0.0, FAKE, FAKE, 1 << 40, FAKE, 1 << 40,
+               None) == 2
+    m = ops.Mask(1, 2, 2, 64, FAKE, FAKE)
+    assert lib.chorus_mask_coverage(ctypes.byref(shp), ctypes.byref(m), None, FAKE, None) == 1
+    assert lib.chorus_mask_coverage(ctypes.byref(shp), ctypes.byref(ops.Mask(1, 3, 2, 64, FAKE, FAKE)),
+                                    FAKE, FAKE, None) == 1
+
