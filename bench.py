@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--coverage", action="store_true",
+                    help="instead of the throughput line, print the mask-coverage study (true block-mass "
+                         "masks of a historical request reused on similar requests)")
     return ap.parse_args()
 
 
@@ -128,12 +131,107 @@ def cpu_baseline(wl, inp, budget_s: float):
             "sample": sample}
 
 
+def coverage_study(args) -> None:
+    """Synthetic analogue of the paper's reuse study (Sec. 3.2 Obs. 1): the
+    true top-p (p = 0.9) block mask of a historical request, taken from its
+    dense attention map, is applied to new requests drawn at increasing
+    distance (noise level sigma) from it, and judged by coverage -- the share
+    of the new request's attention mass inside the mask -- next to the new
+    request's own true mask and the mean-pool predictor built on the new
+    request with its top_p bisected to the same keep ratio.  One JSON line."""
+    import torch
+
+    from paper_2606_25040_amd import ops
+    from paper_2606_25040_amd import workloads as wk
+
+    torch.cuda.set_device(0)
+    ops.load_library()
+    key = args.workload if args.workload != DEFAULT_WORKLOAD else "wan14b_480p_reuse_bf16"
+    wl = wk.WORKLOADS[key]
+    if wl.dtype == "fp8":
+        raise SystemExit("the coverage study runs on the 16-bit workloads")
+    sigmas = [0.1, 0.3, 0.6, 1.0]
+    true_p = 0.9
+    S, sm, mk = wl.S, wl.sm_scale, wl.min_top_k
+    bq, bk, reqs = wk.make_similar_requests(wl, sigmas)
+
+    def event_ms(fn, reps=3):
+        fn()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        e1.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    def mass_of(q, k):
+        qd, kd = q.cuda(), k.cuda()
+        _, lse = ops.block_sparse_attn_fwd(qd, kd, kd, None, sm_scale=sm, return_lse=True)
+        return ops.attn_block_mass(qd, kd, lse, sm_scale=sm), qd, kd, lse
+
+    m_base, qd, kd, lse = mass_of(bq, bk)
+    mass_ms = event_ms(lambda: ops.attn_block_mass(qd, kd, lse, sm_scale=sm, out=m_base))
+    hist = ops.select_block_mask(m_base, S, true_p, mk)
+    select_ms = event_ms(lambda: ops.select_block_mask(m_base, S, true_p, mk, out=hist))
+    pairs = wl.H * wl.n_blocks * wl.n_blocks
+    mass_tflops = pairs * 2 * 64 * 64 * 128 / (mass_ms * 1e-3) / 1e12
+    del qd, kd, lse
+    # the true mask a second time, with its top_p bisected to the workload's
+    # keep ratio (the density the attention kernels are measured at)
+    lo, hi = 0.0, 1.0
+    for _ in range(30):
+        mid = 0.5 * (lo + hi)
+        if ops.select_block_mask(m_base, S, mid, mk).density < wl.density:
+            lo = mid
+        else:
+            hi = mid
+    p_keep = hi
+    hist_keep = ops.select_block_mask(m_base, S, p_keep, mk)
+
+    def bisect_builder(qd, kd, target):
+        lo, hi = 0.0, 1.0
+        for _ in range(24):
+            mid = 0.5 * (lo + hi)
+            if ops.build_block_mask(qd, kd, mid, mk, sm_scale=sm).density < target:
+                lo = mid
+            else:
+                hi = mid
+        return ops.build_block_mask(qd, kd, hi, mk, sm_scale=sm)
+
+    results = []
+    for sig, (q, k) in zip(sigmas, reqs):
+        m_r, qd, kd, _ = mass_of(q, k)
+        row = {"sigma": sig}
+        for tag, p_true, hmask in (("p0.9", true_p, hist), ("keep", p_keep, hist_keep)):
+            own = ops.select_block_mask(m_r, S, p_true, mk)
+            pred = bisect_builder(qd, kd, hmask.density)
+            row[tag] = {"keep_ratio_reused": round(hmask.density, 5),
+                        "keep_ratio_own": round(own.density, 5),
+                        "keep_ratio_meanpool": round(pred.density, 5),
+                        "coverage_own_true_mask": round(float(ops.mask_coverage(own, m_r, S).mean()), 5),
+                        "coverage_reused_true_mask": round(float(ops.mask_coverage(hmask, m_r, S).mean()), 5),
+                        "coverage_meanpool_predictor": round(float(ops.mask_coverage(pred, m_r, S).mean()), 5)}
+        results.append(row)
+        del qd, kd, m_r
+    line = {"study": "mask coverage of a reused true top-p mask (synthetic analogue of Sec. 3.2 Obs. 1)",
+            "workload": key, "true_top_p": true_p, "keep_setting_top_p": round(p_keep, 6), "min_top_k": mk,
+            "data": "synthetic (seeded base request; new requests = base + sigma * N(0,1) on Q and K)",
+            "block_mass_ms": round(mass_ms, 3), "block_mass_tflops": round(mass_tflops, 1),
+            "select_from_mass_ms": round(select_ms, 4), "results": results}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               "(this build measures the single-GPU share of the path).", file=sys.stderr)
         sys.exit(2)
+    if args.coverage:
+        coverage_study(args)
+        return
     import torch
 
     from paper_2606_25040_amd import ops

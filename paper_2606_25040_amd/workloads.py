@@ -189,6 +189,39 @@ def make_inputs(wl: Workload, with_v: bool = True) -> Inputs:
     return Inputs(q, k, v, q, k, None)
 
 
+def make_similar_requests(wl: Workload, sigmas, heads=None):
+    """Q/K of a base (historical) request and of one new request per noise
+    level sigma: Q_s = Q_base + sigma * n_Q, K_s = K_base + sigma * n_K, the
+    noise of level number r drawn from (seed + 1 + r, h) -- the workload's own
+    cross-request recipe with the perturbation made a parameter, so that
+    request similarity can be swept.  Returns ``(base_q, base_k, [(q, k), ...])``,
+    host tensors ``[1, S, len(heads), D]`` in the storage dtype."""
+    S, H, D = wl.S, wl.H, wl.D
+    heads = list(range(H)) if heads is None else list(heads)
+    dt = wl.storage_dtype
+    f = position_features(wl.grid)
+    bq_all = torch.empty((1, S, len(heads), D), dtype=dt)
+    bk_all = torch.empty((1, S, len(heads), D), dtype=dt)
+    reqs = [(torch.empty((1, S, len(heads), D), dtype=dt), torch.empty((1, S, len(heads), D), dtype=dt))
+            for _ in sigmas]
+
+    def head(t: int):
+        h = heads[t]
+        bq, bk, _ = _base_qk(f, wl.seed, h, H, D)
+        bq_all[0, :, t, :].copy_(torch.from_numpy(bq))
+        bk_all[0, :, t, :].copy_(torch.from_numpy(bk))
+        for r, sig in enumerate(sigmas):
+            gr = _stream(wl.seed + 1 + r, h)
+            nq = gr.standard_normal((S, D), dtype=np.float32)
+            nk = gr.standard_normal((S, D), dtype=np.float32)
+            reqs[r][0][0, :, t, :].copy_(torch.from_numpy(bq + np.float32(sig) * nq))
+            reqs[r][1][0, :, t, :].copy_(torch.from_numpy(bk + np.float32(sig) * nk))
+
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(head, range(len(heads))))
+    return bq_all, bk_all, reqs
+
+
 def random_mask(wl: Workload, keep: int | None = None):
     """Fixed random block mask of the tiny check: per (head, q-block) row the
     diagonal block plus ``keep - 1`` distinct others drawn without replacement,

@@ -83,3 +83,19 @@ def test_output_magnitude_fits_bf16_budget():
             sel = om.select_row(s[i], wl.top_p, wl.min_top_k)
             o, _ = oa.attention_block(q[0, :, h], k[0, :, h], v[0, :, h], sel, i, wl.sm_scale)
             assert np.abs(o).max() < 0.5
+
+
+def test_similar_requests_reproduce_the_workload_recipe():
+    """At sigma = 0.3 the swept generator gives exactly the workload's own
+    historical and new requests."""
+    small = wk.Workload("small_reuse", "bf16", 1, 3, (3, 8, 16), 0.2, "historical", 9100)
+    inp = wk.make_inputs(small)
+    bq, bk, reqs = wk.make_similar_requests(small, [0.3, 1.0])
+    assert torch.equal(bq, inp.mask_q) and torch.equal(bk, inp.mask_k)
+    assert torch.equal(reqs[0][0], inp.q) and torch.equal(reqs[0][1], inp.k)
+    # larger sigma moves the request further from the base
+    d03 = (reqs[0][0].float() - bq.float()).pow(2).mean().item()
+    d10 = (reqs[1][0].float() - bq.float()).pow(2).mean().item()
+    assert d10 > 5 * d03
+    sub = wk.make_similar_requests(small, [0.3], heads=[2])
+    assert torch.equal(sub[2][0][0][:, :, 0], inp.q[:, :, 2])
