@@ -21,6 +21,8 @@ Generation"):
   top-k mask selected from it (the masks a historical request records, Sec.
   3.2 "Mask Caching and Retrieval") and the coverage of a mask on a request
   (Sec. 3.2, Obs. 1).
+* ``fallback``   -- block-pair visit refreshing over a layer group, the first
+  safeguard of Sec. 3.2 "Safety fallback against information loss".
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute force,
 closed forms, library routines and invariants.  The one part with no outside
@@ -29,4 +31,4 @@ output or worked example for this path ("parity unpinned" against the paper
 itself; pinned against the mathematics).
 """
 
-from . import attention, fp8, mask, mass  # noqa: F401
+from . import attention, fallback, fp8, mask, mass  # noqa: F401
