@@ -334,6 +334,20 @@ def main():
     build_ms = event_ms(build, reps) if mq is not None else 0.0
     plan_ms = event_ms(lambda: plan(mask), reps)
     quant_ms = event_ms(quant, reps) if fp8 else 0.0
+    # block-pair visit refreshing of a layer group (outside the step: one
+    # update per layer, one refresh at the group's last layer).  The refresh
+    # is timed in its worst case: the map holds only this mask's own pairs,
+    # so every other pair is forced in and the output is dense.
+    vmap = ops.VisitMap(mask.mask_batch, H, n)
+    vmap.reset(mask)
+    refreshed = ops.BlockMask(torch.empty_like(mask.row_ptr),
+                              torch.empty(mask.rows * n, dtype=torch.int32, device="cuda"),
+                              mask.mask_batch, H, n)
+    need = ops.load_library().chorus_visit_refresh_workspace_size(ops.ctypes.byref(mask.as_c()))
+    ws_visit = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
+    visit_update_ms = event_ms(lambda: vmap.update(mask), reps)
+    visit_refresh_ms = event_ms(lambda: vmap.refresh(mask, out=refreshed, workspace=ws_visit), reps)
+    del vmap, refreshed, ws_visit
     dense_reps = max(3, reps // 4)
     dense_ms = event_ms(lambda: attn(mask, None, dense=True), dense_reps)
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
@@ -369,6 +383,8 @@ def main():
         "builder_ms": round(build_ms, 4),
         "plan_ms": round(plan_ms, 4),
         "quant_ms": round(quant_ms, 4),
+        "visit_update_ms": round(visit_update_ms, 4),
+        "visit_refresh_worst_ms": round(visit_refresh_ms, 4),
         "routing_overhead_ratio": round(build_ms / (build_ms + attn_ms), 4),
         "dense_attn_ms": round(dense_ms, 4),
         "speedup_vs_dense": round(dense_ms / attn_ms, 3),

@@ -309,6 +309,43 @@ chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* m
 chorus_status chorus_mask_coverage(const chorus_shape* shape, const chorus_block_mask* mask,
                                    const float* mass, double* coverage, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Block-pair visit refreshing -- Sec. 3.2 "Safety fallback against
+ * information loss", safeguard (1): over a group of layer_flash consecutive
+ * layers (8 in Sec. 4.1) a visited map V records the (head, q-block,
+ * kv-block) pairs the layers' masks activated; at the group's last layer
+ * every pair still unvisited is forced into that layer's mask, so each pair
+ * is touched at least once per group; V is cleared when the next group
+ * starts.  Safeguard (2), the minimum top-k floor, is part of the selection
+ * (min_top_k of chorus_build_block_mask / chorus_select_block_mask).
+ *
+ * V is a caller-owned device bitmap with one bit per (mask row, kv block):
+ * row r = (b_m * H + h) * n_blocks + i owns the words [r * W, (r + 1) * W),
+ * W = ceil(n_blocks / 32), bit j % 32 of word j / 32 is pair (row r, block j).
+ * Its size in bytes is chorus_visit_map_bytes(mask_batch, H, n_blocks).
+ * The three calls below are stream-ordered; V must not be shared by calls
+ * running concurrently on different streams.
+ *
+ * chorus_visit_reset   : V = {} (a fill kernel, no memset).
+ * chorus_visit_update  : V |= pairs of mask (a layer inside the group).
+ * chorus_visit_refresh : writes the group's last-layer mask
+ *                        out = mask | ~V (per row, the blocks of the mask
+ *                        plus every block V has not recorded), as a CSR
+ *                        with the mask's mask_batch / H / n_blocks; ids
+ *                        ascending.  V is not modified (call
+ *                        chorus_visit_update with the output to record it).
+ *   row_ptr, col_idx, col_capacity : as chorus_build_block_mask
+ *                        (col_capacity >= rows * n_blocks).
+ *   workspace : chorus_visit_refresh_workspace_size(mask) bytes, 256-aligned.
+ * ------------------------------------------------------------------------- */
+size_t chorus_visit_map_bytes(int32_t mask_batch, int32_t H, int32_t n_blocks);
+chorus_status chorus_visit_reset(const chorus_block_mask* mask, uint32_t* visited, void* stream);
+chorus_status chorus_visit_update(const chorus_block_mask* mask, uint32_t* visited, void* stream);
+size_t chorus_visit_refresh_workspace_size(const chorus_block_mask* mask);
+chorus_status chorus_visit_refresh(const chorus_block_mask* mask, const uint32_t* visited,
+                                   int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
 /* Human-readable name of a status, and the detail of the calling thread's
  * last error (empty string if none).  Both return static / thread-local
  * storage owned by the library. */

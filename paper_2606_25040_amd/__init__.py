@@ -8,6 +8,7 @@ and fails loudly if it has not been built.
 
 from .ops import (  # noqa: F401
     BlockMask,
+    VisitMap,
     attn_block_mass,
     block_sparse_attn_fwd,
     block_sparse_attn_fwd_bf16,

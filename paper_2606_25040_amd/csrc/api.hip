@@ -400,4 +400,77 @@ chorus_status chorus_mask_coverage(const chorus_shape* shape, const chorus_block
                   "coverage");
 }
 
+static chorus_status check_mask_alone(const chorus_block_mask* m) {
+  if (!m) return fail(CHORUS_ERR_INVALID_ARG, "mask is NULL");
+  if (m->block != kBlock) return fail(CHORUS_ERR_UNSUPPORTED, "mask block %d unsupported (only 64)", m->block);
+  if (m->mask_batch < 1 || m->H < 1 || m->n_blocks < 1)
+    return fail(CHORUS_ERR_INVALID_ARG, "mask_batch/H/n_blocks must be >= 1");
+  if (m->n_blocks > kMaxBuilderBlocks)
+    return fail(CHORUS_ERR_UNSUPPORTED, "n_blocks=%d exceeds limit %d", m->n_blocks, kMaxBuilderBlocks);
+  if (!m->row_ptr || !m->col_idx) return fail(CHORUS_ERR_INVALID_ARG, "mask row_ptr/col_idx is NULL");
+  return CHORUS_OK;
+}
+
+size_t chorus_visit_map_bytes(int32_t mask_batch, int32_t H, int32_t n_blocks) {
+  if (mask_batch < 1 || H < 1 || n_blocks < 1) return 0;
+  return (size_t)mask_batch * H * n_blocks * ((n_blocks + 31) / 32) * sizeof(uint32_t);
+}
+
+chorus_status chorus_visit_reset(const chorus_block_mask* mask, uint32_t* visited, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_mask_alone(mask))) return st;
+  if (!visited) return fail(CHORUS_ERR_INVALID_ARG, "visited is NULL");
+  const int64_t words = (int64_t)mask->mask_batch * mask->H * mask->n_blocks * ((mask->n_blocks + 31) / 32);
+  return from_hip(launch_fill_u32(visited, 0u, words, static_cast<hipStream_t>(stream)), "visit_reset");
+}
+
+chorus_status chorus_visit_update(const chorus_block_mask* mask, uint32_t* visited, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_mask_alone(mask))) return st;
+  if (!visited) return fail(CHORUS_ERR_INVALID_ARG, "visited is NULL");
+  const int64_t rows = (int64_t)mask->mask_batch * mask->H * mask->n_blocks;
+  return from_hip(launch_visit_update(mask->row_ptr, mask->col_idx, rows, mask->n_blocks, visited,
+                                      static_cast<hipStream_t>(stream)),
+                  "visit_update");
+}
+
+size_t chorus_visit_refresh_workspace_size(const chorus_block_mask* mask) {
+  if (!mask || mask->mask_batch < 1 || mask->H < 1 || mask->n_blocks < 1) return 0;
+  const size_t rows = (size_t)mask->mask_batch * mask->H * mask->n_blocks;
+  Carver c(nullptr);
+  c.take<int32_t>(rows);
+  c.take<uint32_t>(rows * ((mask->n_blocks + 31) / 32));
+  return align_up(c.used, 256);
+}
+
+chorus_status chorus_visit_refresh(const chorus_block_mask* mask, const uint32_t* visited,
+                                   int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_mask_alone(mask))) return st;
+  if (!visited) return fail(CHORUS_ERR_INVALID_ARG, "visited is NULL");
+  if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
+  const int n = mask->n_blocks;
+  const int64_t rows = (int64_t)mask->mask_batch * mask->H * n;
+  if (rows * n > INT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "rows*n_blocks = %lld exceeds int32 CSR offsets", (long long)(rows * n));
+  if (col_capacity < rows * n)
+    return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
+                (long long)(rows * n));
+  if ((st = check_workspace(workspace, workspace_bytes, chorus_visit_refresh_workspace_size(mask)))) return st;
+  Carver c(workspace);
+  int32_t* counts = c.take<int32_t>(rows);
+  const int words = (n + 31) / 32;
+  uint32_t* bitmap = c.take<uint32_t>(rows * words);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = from_hip(launch_visit_refresh(mask->row_ptr, mask->col_idx, rows, n, visited, counts, bitmap, s),
+                     "visit_refresh")))
+    return st;
+  if ((st = from_hip(launch_scan_counts(counts, rows, row_ptr, s), "scan"))) return st;
+  return from_hip(launch_compact(bitmap, words, row_ptr, rows, col_idx, s), "compact");
+}
+
 }  // extern "C"

@@ -74,6 +74,13 @@ hipError_t launch_block_mass(chorus_dtype dt, TensorArg q, TensorArg k, const fl
 hipError_t launch_coverage(const int32_t* row_ptr, const int32_t* col_idx, int mask_batch, const float* mass, int B,
                            int S, int H, double* coverage, hipStream_t st);
 
+// ---- visit refreshing (fallback.hip) ----
+hipError_t launch_visit_update(const int32_t* row_ptr, const int32_t* col_idx, int64_t rows, int n,
+                               uint32_t* visited, hipStream_t st);
+hipError_t launch_visit_refresh(const int32_t* row_ptr, const int32_t* col_idx, int64_t rows, int n,
+                                const uint32_t* visited, int32_t* counts, uint32_t* bitmap, hipStream_t st);
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t count, hipStream_t st);
+
 // ---- fp8 quantiser (quant_fp8.hip) ----
 hipError_t launch_quant_fp8(chorus_dtype in_dt, TensorArg x, TensorArg codes, int B, int S, int H,
                             float* scales, hipStream_t st);

@@ -720,7 +720,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __res
 
 // ---------------------------------------------------------------------------
 // 4. Compact each row's bitmap into ascending col_idx (one wave per row; each
-// lane owns up to two consecutive 32-bit words, so n <= 4096).
+// lane holds two consecutive 32-bit words, so n <= 4096).  The row is walked
+// 64 blocks at a time: lane l owns block 64 c + l of chunk c and writes it at
+// the chunk's base plus the number of set bits below it, so every store of
+// the wave is contiguous whatever the row's density.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict__ bitmap, int words,
                                                       const int32_t* __restrict__ row_ptr, int64_t rows,
@@ -732,24 +735,14 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict
   const int w0 = 2 * lane, w1 = 2 * lane + 1;
   const uint32_t a = w0 < words ? src[w0] : 0u;
   const uint32_t c = w1 < words ? src[w1] : 0u;
-  const int cnt = __popc(a) + __popc(c);
-  int incl = cnt;
-  for (int o = 1; o < 64; o <<= 1) {
-    const int v = __shfl_up(incl, o);
-    if (lane >= o) incl += v;
-  }
-  int pos = row_ptr[row] + incl - cnt;
-  uint32_t x = a;
-  while (x) {
-    const int bit = __ffs(x) - 1;
-    col_idx[pos++] = w0 * 32 + bit;
-    x &= x - 1;
-  }
-  x = c;
-  while (x) {
-    const int bit = __ffs(x) - 1;
-    col_idx[pos++] = w1 * 32 + bit;
-    x &= x - 1;
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  int32_t* dst = col_idx + row_ptr[row];
+  const int chunks = (words + 1) / 2;
+  for (int ch = 0; ch < chunks; ++ch) {
+    const uint64_t bits = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)a, ch) |
+                          ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)c, ch) << 32);
+    if ((bits >> lane) & 1ull) dst[__popcll(bits & below)] = ch * 64 + lane;
+    dst += __popcll(bits);
   }
 }
 

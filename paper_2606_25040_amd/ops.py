@@ -54,6 +54,8 @@ EXPORTS = [
     "chorus_block_sparse_attn_fwd_bf16", "chorus_block_sparse_attn_fwd_fp8",
     "chorus_attn_block_mass", "chorus_select_block_mask_workspace_size", "chorus_select_block_mask",
     "chorus_mask_coverage",
+    "chorus_visit_map_bytes", "chorus_visit_reset", "chorus_visit_update",
+    "chorus_visit_refresh_workspace_size", "chorus_visit_refresh",
     "chorus_status_string", "chorus_last_error", "chorus_version",
 ]
 
@@ -96,6 +98,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "chorus_select_block_mask_workspace_size": (SZ, [P(Shape)]),
         "chorus_select_block_mask": (I32, [P(Shape), VP, F64, F64, VP, VP, I64, VP, SZ, VP]),
         "chorus_mask_coverage": (I32, [P(Shape), P(Mask), VP, VP, VP]),
+        "chorus_visit_map_bytes": (SZ, [I32, I32, I32]),
+        "chorus_visit_reset": (I32, [P(Mask), VP, VP]),
+        "chorus_visit_update": (I32, [P(Mask), VP, VP]),
+        "chorus_visit_refresh_workspace_size": (SZ, [P(Mask)]),
+        "chorus_visit_refresh": (I32, [P(Mask), VP, VP, VP, I64, VP, SZ, VP]),
         "chorus_status_string": (ctypes.c_char_p, [I32]),
         "chorus_last_error": (ctypes.c_char_p, []),
         "chorus_version": (I32, []),
@@ -386,3 +393,55 @@ def mask_coverage(mask: BlockMask, mass: torch.Tensor, S: int) -> torch.Tensor:
                                 cov.data_ptr(), _stream())
     _check(st, "chorus_mask_coverage")
     return cov
+
+
+class VisitMap:
+    """Device visited bitmap of a layer group (chorus_visit_*), sized for
+    masks with the given mask_batch / H / n_blocks."""
+
+    def __init__(self, mask_batch: int, H: int, n_blocks: int, device="cuda"):
+        L = load_library()
+        nbytes = L.chorus_visit_map_bytes(mask_batch, H, n_blocks)
+        self.mask_batch, self.H, self.n_blocks = mask_batch, H, n_blocks
+        self.words = (n_blocks + 31) // 32
+        self.bits = torch.empty(nbytes // 4, dtype=torch.int32, device=device)
+
+    def _check_mask(self, mask: BlockMask):
+        if (mask.mask_batch, mask.H, mask.n_blocks) != (self.mask_batch, self.H, self.n_blocks):
+            raise ValueError("mask dimensions differ from the visited map's")
+
+    def reset(self, like: BlockMask):
+        self._check_mask(like)
+        st = load_library().chorus_visit_reset(ctypes.byref(like.as_c()), self.bits.data_ptr(), _stream())
+        _check(st, "chorus_visit_reset")
+
+    def update(self, mask: BlockMask):
+        self._check_mask(mask)
+        st = load_library().chorus_visit_update(ctypes.byref(mask.as_c()), self.bits.data_ptr(), _stream())
+        _check(st, "chorus_visit_update")
+
+    def refresh(self, mask: BlockMask, out: BlockMask | None = None,
+                workspace: torch.Tensor | None = None) -> BlockMask:
+        """The group's last-layer mask: mask | (pairs not visited)."""
+        self._check_mask(mask)
+        L = load_library()
+        rows = mask.rows
+        n = mask.n_blocks
+        m = out if out is not None else BlockMask(
+            torch.empty(rows + 1, dtype=torch.int32, device=self.bits.device),
+            torch.empty(rows * n, dtype=torch.int32, device=self.bits.device), mask.mask_batch, mask.H, n)
+        cm = mask.as_c()
+        need = L.chorus_visit_refresh_workspace_size(ctypes.byref(cm))
+        ws = workspace if workspace is not None and workspace.numel() >= need + 256 else \
+            _workspace(need, self.bits.device)
+        st = L.chorus_visit_refresh(ctypes.byref(cm), self.bits.data_ptr(), m.row_ptr.data_ptr(),
+                                    m.col_idx.data_ptr(), m.col_idx.numel(), _aligned(ws), need, _stream())
+        _check(st, "chorus_visit_refresh")
+        return m
+
+    def to_host(self):
+        """Boolean [rows, n_blocks] numpy view of the map."""
+        import numpy as np
+        w = self.bits.cpu().numpy().view(np.uint32).reshape(-1, self.words)
+        bits = ((w[:, :, None] >> np.arange(32, dtype=np.uint32)) & 1).astype(bool)
+        return bits.reshape(w.shape[0], -1)[:, : self.n_blocks]

@@ -140,3 +140,19 @@ def test_block_mass_selection_and_coverage_check_arguments(lib):
     assert lib.chorus_mask_coverage(ctypes.byref(shp), ctypes.byref(ops.Mask(1, 3, 2, 64, FAKE, FAKE)),
                                     FAKE, FAKE, None) == 1
 
+
+
+def test_visit_refresh_checks_arguments(lib):
+    assert lib.chorus_visit_map_bytes(1, 40, 1182) == 40 * 1182 * 37 * 4
+    assert lib.chorus_visit_map_bytes(0, 40, 1182) == 0
+    m = ops.Mask(1, 2, 10, 64, FAKE, FAKE)
+    assert lib.chorus_visit_refresh_workspace_size(ctypes.byref(m)) >= 20 * 4 + 20 * 4
+    assert lib.chorus_visit_reset(None, FAKE, None) == 1
+    assert lib.chorus_visit_update(ctypes.byref(m), None, None) == 1
+    assert lib.chorus_visit_update(ctypes.byref(ops.Mask(1, 2, 10, 128, FAKE, FAKE)), FAKE, None) == 2
+    assert lib.chorus_visit_update(ctypes.byref(ops.Mask(1, 2, 4097, 64, FAKE, FAKE)), FAKE, None) == 2
+    assert lib.chorus_visit_update(ctypes.byref(ops.Mask(1, 2, 10, 64, None, FAKE)), FAKE, None) == 1
+    need = lib.chorus_visit_refresh_workspace_size(ctypes.byref(m))
+    assert lib.chorus_visit_refresh(ctypes.byref(m), FAKE, FAKE, FAKE, 2 * 10 * 10 - 1, FAKE, need, None) == 3
+    assert lib.chorus_visit_refresh(ctypes.byref(m), FAKE, FAKE, FAKE, 2 * 10 * 10, FAKE, need - 4, None) == 5
+    assert lib.chorus_visit_refresh(ctypes.byref(m), None, FAKE, FAKE, 2 * 10 * 10, FAKE, need, None) == 1
