@@ -23,6 +23,8 @@ Generation"):
   (Sec. 3.2, Obs. 1).
 * ``fallback``   -- block-pair visit refreshing over a layer group, the first
   safeguard of Sec. 3.2 "Safety fallback against information loss".
+* ``guidance``   -- the first-frame key enhancement of Eq. (1) (Sec. 3.4),
+  applied to K before any of the above.
 
 Every function is pinned by ``tests/test_oracle_*.py`` against brute force,
 closed forms, library routines and invariants.  The one part with no outside
@@ -31,4 +33,4 @@ output or worked example for this path ("parity unpinned" against the paper
 itself; pinned against the mathematics).
 """
 
-from . import attention, fallback, fp8, mask, mass  # noqa: F401
+from . import attention, fallback, fp8, guidance, mask, mass  # noqa: F401
