@@ -285,13 +285,14 @@ def main():
         for x, c, s in zip((q, k, v), codes, scales):
             ops.quantize_fp8_blockwise(x, codes=c, scales=s)
 
-    def attn(m, sched, dense=False):
+    def attn(m, sched, dense=False, key_scale=None):
         mm = None if dense else m
         if fp8:
             return ops.block_sparse_attn_fwd(codes[0], codes[1], codes[2], mm, sm_scale=wl.sm_scale,
-                                             scales=tuple(scales), out=out, schedule=sched)
+                                             scales=tuple(scales), out=out, schedule=sched,
+                                             key_scale=key_scale)
         return ops.block_sparse_attn_fwd(q, k, v, mm, sm_scale=wl.sm_scale, out=out,
-                                         schedule=sched)
+                                         schedule=sched, key_scale=key_scale)
 
     def step():
         m = build()
@@ -331,6 +332,10 @@ def main():
 
     reps = max(args.steps, 10)
     attn_ms = event_ms(lambda: attn(mask, sched), reps)
+    # the same launch with the first-frame key enhancement (first latent frame
+    # = grid_y * grid_x tokens, beta 1.3)
+    first_frame = wl.grid[1] * wl.grid[2]
+    attn_ks_ms = event_ms(lambda: attn(mask, sched, key_scale=(first_frame, 1.3)), reps)
     build_ms = event_ms(build, reps) if mq is not None else 0.0
     plan_ms = event_ms(lambda: plan(mask), reps)
     quant_ms = event_ms(quant, reps) if fp8 else 0.0
@@ -380,6 +385,7 @@ def main():
         "attn_ms": round(attn_ms, 4),
         "attn_tflops": round(attn_tflops, 2),
         "attn_frac_mfma_peak": round(attn_tflops / peak, 4),
+        "attn_key_scaled_ms": round(attn_ks_ms, 4),
         "builder_ms": round(build_ms, 4),
         "plan_ms": round(plan_ms, 4),
         "quant_ms": round(quant_ms, 4),

@@ -99,6 +99,24 @@ typedef struct {
 } chorus_schedule;
 
 /* ---------------------------------------------------------------------------
+ * First-frame key enhancement -- Sec. 3.4 "Guidance Enhancement", Eq. (1):
+ * after the QKV projection the keys of the first frame's tokens are
+ * multiplied by a step-dependent factor beta (Q and V unchanged):
+ *   K[b, c, h, :] <- beta * K[b, c, h, :]   for every token c < n_first,
+ * n_first = H_patch * W_patch.  The calls that take a key_scale apply it on
+ * the fly and never write K: the attention kernels and the block mass
+ * multiply the logits of those keys by beta (a logit is linear in its key);
+ * the mask builder multiplies their contribution to the pooled key.  NULL,
+ * n_first = 0 or beta = 1 is the plain path.  Requires 0 <= n_first <= S and
+ * a finite beta, else CHORUS_ERR_INVALID_ARG.  The schedule of beta over
+ * sampling steps is the caller's.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int32_t n_first;
+  float beta;
+} chorus_key_scale;
+
+/* ---------------------------------------------------------------------------
  * Mask builder -- Sec. 3.2 Obs. 2 (score = softmax(mean(Q) mean(K)^T)),
  * Sec. 3.2 "Mask Caching and Retrieval" (top-p with a top-k floor), Sec. 3.2
  * "Minimum top-k guarantee", Sec. 4.1 (top_p, min_top_k).
@@ -116,6 +134,8 @@ typedef struct {
  *      and writes them ascending as CSR row (b * H + h) * n_blocks + i.
  * The result has mask_batch = B.  To build one mask from one request (and
  * reuse it for others), pass a B = 1 view of that request.
+ * key_scale     : optional first-frame key enhancement (NULL for none): the
+ *                 pooled keys are those of the scaled K.
  *
  * q, k          : [B, S, H, D] f16 or bf16 (dtype), read only.
  * row_ptr       : out, device int32 [B * H * n_blocks + 1].
@@ -133,6 +153,7 @@ size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape);
 chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
                                       const chorus_tensor* q, const chorus_tensor* k,
                                       double sm_scale, double top_p, double min_top_k,
+                                      const chorus_key_scale* key_scale,
                                       int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
                                       float* block_scores, void* workspace,
                                       size_t workspace_bytes, void* stream);
@@ -207,6 +228,9 @@ chorus_status chorus_quantize_fp8_blockwise(chorus_dtype in_dtype, const chorus_
  * lse      : optional out (NULL to skip), device float32 [B, H, S] contiguous.
  * schedule : optional work order from chorus_plan_block_mask (NULL = the
  *            library's default order); never changes results.
+ * key_scale: optional first-frame key enhancement (NULL for none): the
+ *            logits of keys c < n_first are multiplied by beta, as if K had
+ *            been scaled by Eq. (1) (for fp8: the dequantised keys).
  * workspace: device scratch of chorus_attn_workspace_size() bytes (may be 0).
  * Results are bitwise deterministic for a given input, mask and dtype.
  * ------------------------------------------------------------------------- */
@@ -218,6 +242,7 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
                                            const float* k_scale, const float* v_scale,
                                            const chorus_block_mask* mask,
                                            const chorus_schedule* schedule, float sm_scale,
+                                           const chorus_key_scale* key_scale,
                                            const chorus_tensor* out, float* lse, void* workspace,
                                            size_t workspace_bytes, void* stream);
 
@@ -226,6 +251,7 @@ chorus_status chorus_block_sparse_attn_fwd_f16(const chorus_shape* shape, const 
                                                const chorus_tensor* k, const chorus_tensor* v,
                                                const chorus_block_mask* mask,
                                                const chorus_schedule* schedule, float sm_scale,
+                                               const chorus_key_scale* key_scale,
                                                const chorus_tensor* out, float* lse,
                                                void* workspace, size_t workspace_bytes,
                                                void* stream);
@@ -233,6 +259,7 @@ chorus_status chorus_block_sparse_attn_fwd_bf16(const chorus_shape* shape, const
                                                 const chorus_tensor* k, const chorus_tensor* v,
                                                 const chorus_block_mask* mask,
                                                 const chorus_schedule* schedule, float sm_scale,
+                                                const chorus_key_scale* key_scale,
                                                 const chorus_tensor* out, float* lse,
                                                 void* workspace, size_t workspace_bytes,
                                                 void* stream);
@@ -242,6 +269,7 @@ chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const 
                                                const float* v_scale,
                                                const chorus_block_mask* mask,
                                                const chorus_schedule* schedule, float sm_scale,
+                                               const chorus_key_scale* key_scale,
                                                const chorus_tensor* out, float* lse,
                                                void* workspace, size_t workspace_bytes,
                                                void* stream);
@@ -263,11 +291,14 @@ chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const 
  *
  * q, k  : [B, S, H, D] f16 or bf16 (dtype), read only.
  * lse   : device float32 [B, H, S], read only.
+ * key_scale : optional first-frame key enhancement (NULL for none), as in
+ *         the dense pass that wrote lse.
  * mass  : out, device float32 [B, H, n_blocks, n_blocks], row-major.
  * ------------------------------------------------------------------------- */
 chorus_status chorus_attn_block_mass(chorus_dtype dtype, const chorus_shape* shape,
                                      const chorus_tensor* q, const chorus_tensor* k, const float* lse,
-                                     float sm_scale, float* mass, void* stream);
+                                     float sm_scale, const chorus_key_scale* key_scale, float* mass,
+                                     void* stream);
 
 /* ---------------------------------------------------------------------------
  * Block mask from block masses (the selection of Sec. 3.2 "Mask Caching and

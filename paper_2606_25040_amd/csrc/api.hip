@@ -78,6 +78,21 @@ static chorus_status check_mask(const chorus_shape* s, const chorus_block_mask* 
   return CHORUS_OK;
 }
 
+// Copies an optional key scale; NULL, n_first == 0 or beta == 1 turn it off.
+static chorus_status check_key_scale(const chorus_key_scale* ks, int S, KeyScale* out) {
+  out->n_first = 0;
+  out->beta = 1.f;
+  if (!ks) return CHORUS_OK;
+  if (ks->n_first < 0 || ks->n_first > S)
+    return fail(CHORUS_ERR_INVALID_ARG, "key_scale n_first=%d outside [0, S=%d]", ks->n_first, S);
+  if (!std::isfinite(ks->beta)) return fail(CHORUS_ERR_INVALID_ARG, "key_scale beta must be finite");
+  if (ks->n_first > 0 && ks->beta != 1.f) {
+    out->n_first = ks->n_first;
+    out->beta = ks->beta;
+  }
+  return CHORUS_OK;
+}
+
 static chorus_status check_workspace(void* ws, size_t have, size_t need) {
   if (need == 0) return CHORUS_OK;
   if (!ws) return fail(CHORUS_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
@@ -132,6 +147,7 @@ size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape) {
 chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
                                       const chorus_tensor* q, const chorus_tensor* k,
                                       double sm_scale, double top_p, double min_top_k,
+                                      const chorus_key_scale* key_scale,
                                       int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
                                       float* block_scores, void* workspace,
                                       size_t workspace_bytes, void* stream) {
@@ -149,6 +165,8 @@ chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* sh
   if (!(min_top_k >= 0.0 && min_top_k <= 1.0))
     return fail(CHORUS_ERR_INVALID_ARG, "min_top_k must be in [0, 1]");
   if (!std::isfinite(sm_scale)) return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite");
+  KeyScale ks;
+  if ((st = check_key_scale(key_scale, shape->S, &ks))) return st;
   if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
   const int64_t rows = (int64_t)shape->B * shape->H * n;
   if (rows * n > INT32_MAX)
@@ -161,7 +179,7 @@ chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* sh
   if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
   const int k_min = (int)std::ceil(min_top_k * (double)n - 1e-9);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = from_hip(launch_pool(dtype, targ(q), targ(k), shape->B, shape->S, shape->H, w.qbar, w.kbar, s),
+  if ((st = from_hip(launch_pool(dtype, targ(q), targ(k), shape->B, shape->S, shape->H, ks, w.qbar, w.kbar, s),
                      "pool")))
     return st;
   if ((st = from_hip(launch_score_select(w.qbar, w.kbar, shape->B, shape->H, n, sm_scale, top_p,
@@ -234,6 +252,7 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
                                            const float* k_scale, const float* v_scale,
                                            const chorus_block_mask* mask,
                                            const chorus_schedule* schedule, float sm_scale,
+                                           const chorus_key_scale* key_scale,
                                            const chorus_tensor* out, float* lse, void* workspace,
                                            size_t workspace_bytes, void* stream) {
   g_last_error[0] = 0;
@@ -255,6 +274,8 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   }
   if (!std::isfinite(sm_scale) || !(sm_scale > 0.f))
     return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite and > 0");
+  KeyScale ks;
+  if ((st = check_key_scale(key_scale, shape->S, &ks))) return st;
   const int n = blocks_of(shape->S);
   const int64_t items = (int64_t)shape->B * shape->H * n;
   if (items > INT32_MAX) return fail(CHORUS_ERR_UNSUPPORTED, "too many work items");
@@ -286,6 +307,7 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   a.H = shape->H;
   a.n = n;
   a.sm_scale = sm_scale;
+  a.ks = ks;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == CHORUS_FP8_E4M3) return from_hip(launch_attn_fwd_fp8(a, s), "attn_fwd_fp8");
   return from_hip(launch_attn_fwd_16(dtype, a, s), "attn_fwd");
@@ -295,20 +317,22 @@ chorus_status chorus_block_sparse_attn_fwd_f16(const chorus_shape* shape, const 
                                                const chorus_tensor* k, const chorus_tensor* v,
                                                const chorus_block_mask* mask,
                                                const chorus_schedule* schedule, float sm_scale,
+                                               const chorus_key_scale* key_scale,
                                                const chorus_tensor* out, float* lse, void* workspace,
                                                size_t workspace_bytes, void* stream) {
   return chorus_block_sparse_attn_fwd(CHORUS_F16, shape, q, k, v, nullptr, nullptr, nullptr, mask, schedule,
-                                      sm_scale, out, lse, workspace, workspace_bytes, stream);
+                                      sm_scale, key_scale, out, lse, workspace, workspace_bytes, stream);
 }
 
 chorus_status chorus_block_sparse_attn_fwd_bf16(const chorus_shape* shape, const chorus_tensor* q,
                                                 const chorus_tensor* k, const chorus_tensor* v,
                                                 const chorus_block_mask* mask,
                                                 const chorus_schedule* schedule, float sm_scale,
+                                                const chorus_key_scale* key_scale,
                                                 const chorus_tensor* out, float* lse, void* workspace,
                                                 size_t workspace_bytes, void* stream) {
   return chorus_block_sparse_attn_fwd(CHORUS_BF16, shape, q, k, v, nullptr, nullptr, nullptr, mask, schedule,
-                                      sm_scale, out, lse, workspace, workspace_bytes, stream);
+                                      sm_scale, key_scale, out, lse, workspace, workspace_bytes, stream);
 }
 
 chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const chorus_tensor* q,
@@ -316,15 +340,18 @@ chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const 
                                                const float* q_scale, const float* k_scale,
                                                const float* v_scale, const chorus_block_mask* mask,
                                                const chorus_schedule* schedule, float sm_scale,
+                                               const chorus_key_scale* key_scale,
                                                const chorus_tensor* out, float* lse, void* workspace,
                                                size_t workspace_bytes, void* stream) {
   return chorus_block_sparse_attn_fwd(CHORUS_FP8_E4M3, shape, q, k, v, q_scale, k_scale, v_scale, mask,
-                                      schedule, sm_scale, out, lse, workspace, workspace_bytes, stream);
+                                      schedule, sm_scale, key_scale, out, lse, workspace, workspace_bytes,
+                                      stream);
 }
 
 chorus_status chorus_attn_block_mass(chorus_dtype dtype, const chorus_shape* shape,
                                      const chorus_tensor* q, const chorus_tensor* k, const float* lse,
-                                     float sm_scale, float* mass, void* stream) {
+                                     float sm_scale, const chorus_key_scale* key_scale, float* mass,
+                                     void* stream) {
   g_last_error[0] = 0;
   chorus_status st;
   if ((st = check_shape(shape))) return st;
@@ -338,7 +365,9 @@ chorus_status chorus_attn_block_mass(chorus_dtype dtype, const chorus_shape* sha
   if (!offsets_fit(shape->S, k->stride_s, 2))
     return fail(CHORUS_ERR_UNSUPPORTED, "token stride too large for 32-bit in-head offsets");
   if (shape->H > 65535 || shape->B > 65535) return fail(CHORUS_ERR_UNSUPPORTED, "B or H above 65535");
-  return from_hip(launch_block_mass(dtype, targ(q), targ(k), lse, shape->B, shape->S, shape->H, sm_scale, mass,
+  KeyScale ks;
+  if ((st = check_key_scale(key_scale, shape->S, &ks))) return st;
+  return from_hip(launch_block_mass(dtype, targ(q), targ(k), lse, shape->B, shape->S, shape->H, sm_scale, ks, mass,
                                     static_cast<hipStream_t>(stream)),
                   "block_mass");
 }

@@ -109,7 +109,7 @@ struct TileLoader {
   }
 };
 
-template <bool BF16, bool DENSE>
+template <bool BF16, bool DENSE, bool KSCALE>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
   using E = Elt<BF16>;
@@ -223,6 +223,17 @@ void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
     __syncthreads();                               // every wave is done with K_j
     if (has_next) kl.load<true>(k_s, j_next, S, wave);
 
+    // first-frame keys (Eq. 1): their logits count beta times
+    if (KSCALE && j * kBlock < a.ks.n_first) {
+      const int lim = a.ks.n_first - j * kBlock;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = 32 * t + 8 * (r >> 2) + 4 * hl + (r & 3);
+          if (key < lim) sacc[t][r] *= a.ks.beta;
+        }
+    }
     // keys at or beyond S (partial last block) carry no weight
     if (j * kBlock + kBlock > S) {
 #pragma unroll
@@ -313,21 +324,31 @@ void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
 
 }  // namespace
 
+namespace {
+template <bool BF16, bool DENSE>
+void launch_16(const AttnArgs& a, dim3 grid, int chunk, int W, hipStream_t st) {
+  if (a.ks.n_first > 0)
+    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, true>), grid, dim3(128), 0, st, a, chunk, W);
+  else
+    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, false>), grid, dim3(128), 0, st, a, chunk, W);
+}
+}  // namespace
+
 hipError_t launch_attn_fwd_16(chorus_dtype dt, const AttnArgs& a, hipStream_t st) {
   const int W = a.B * a.H * a.n;
   const int chunk = (W + kNumXcd - 1) / kNumXcd;
-  const dim3 grid(chunk * kNumXcd), block(128);
+  const dim3 grid(chunk * kNumXcd);
   const bool dense = a.row_ptr == nullptr;
   if (dt == CHORUS_BF16) {
     if (dense)
-      hipLaunchKernelGGL((attn_fwd_16_kernel<true, true>), grid, block, 0, st, a, chunk, W);
+      launch_16<true, true>(a, grid, chunk, W, st);
     else
-      hipLaunchKernelGGL((attn_fwd_16_kernel<true, false>), grid, block, 0, st, a, chunk, W);
+      launch_16<true, false>(a, grid, chunk, W, st);
   } else {
     if (dense)
-      hipLaunchKernelGGL((attn_fwd_16_kernel<false, true>), grid, block, 0, st, a, chunk, W);
+      launch_16<false, true>(a, grid, chunk, W, st);
     else
-      hipLaunchKernelGGL((attn_fwd_16_kernel<false, false>), grid, block, 0, st, a, chunk, W);
+      launch_16<false, false>(a, grid, chunk, W, st);
   }
   return hipGetLastError();
 }

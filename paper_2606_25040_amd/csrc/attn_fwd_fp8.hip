@@ -59,7 +59,7 @@ __device__ inline void load_tile8(uint32_t lds, const char* base, uint32_t ss, i
   }
 }
 
-template <bool DENSE>
+template <bool DENSE, bool KSCALE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
   __shared__ __attribute__((aligned(1024))) uint8_t tiles[2][2][kTile8];   // [buffer][K, V]
@@ -180,6 +180,15 @@ void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
           sacc[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf, qf[s], sacc[t], 0, 0, 0, 127, 0, 127);
         }
       }
+      // first-frame keys (Eq. 1, on the dequantised keys): logits count beta times
+      if (KSCALE && j * kBlock < a.ks.n_first) {
+        const int lim = a.ks.n_first - j * kBlock;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (32 * t + 16 * hl + r < lim) sacc[t][r] *= a.ks.beta;
+      }
       if (j * kBlock + kBlock > S) {
 #pragma unroll
         for (int t = 0; t < 2; ++t)
@@ -273,10 +282,18 @@ hipError_t launch_attn_fwd_fp8(const AttnArgs& a, hipStream_t st) {
   const int W = a.B * a.H * np;
   const int chunk = (W + kNumXcd - 1) / kNumXcd;
   const dim3 grid(chunk * kNumXcd), block(64 * kWaves);
-  if (a.row_ptr == nullptr)
-    hipLaunchKernelGGL(attn_fwd_fp8_kernel<true>, grid, block, 0, st, a, chunk, W, np);
-  else
-    hipLaunchKernelGGL(attn_fwd_fp8_kernel<false>, grid, block, 0, st, a, chunk, W, np);
+  const bool ks = a.ks.n_first > 0;
+  if (a.row_ptr == nullptr) {
+    if (ks)
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, true>), grid, block, 0, st, a, chunk, W, np);
+    else
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, false>), grid, block, 0, st, a, chunk, W, np);
+  } else {
+    if (ks)
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, true>), grid, block, 0, st, a, chunk, W, np);
+    else
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, false>), grid, block, 0, st, a, chunk, W, np);
+  }
   return hipGetLastError();
 }
 

@@ -56,7 +56,7 @@ __device__ inline void load_k_half(uint32_t lds, const char* base, uint32_t ss, 
 template <bool BF16>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 void block_mass_kernel(TensorArg q, TensorArg k, const float* __restrict__ lse, int S, int H, int n,
-                       float sm_scale, float* __restrict__ mass) {
+                       float sm_scale, KeyScale ks, float* __restrict__ mass) {
   using E = MassElt<BF16>;
   using vec8 = typename E::vec8;
   using scalar = typename E::scalar;
@@ -116,6 +116,15 @@ void block_mass_kernel(TensorArg q, TensorArg k, const float* __restrict__ lse, 
         sacc[t] = E::mfma(kf, qf[s], sacc[t]);
       }
     }
+    // first-frame keys (Eq. 1): their logits count beta times
+    if (j * kBlock < ks.n_first) {
+      const int lim = ks.n_first - j * kBlock;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (32 * t + 8 * (r >> 2) + 4 * hl + (r & 3) < lim) sacc[t][r] *= ks.beta;
+    }
     float sum = 0.f;
     const bool partial = j * kBlock + kBlock > S;
 #pragma unroll
@@ -165,13 +174,13 @@ __global__ __launch_bounds__(256) void coverage_kernel(const int32_t* __restrict
 }  // namespace
 
 hipError_t launch_block_mass(chorus_dtype dt, TensorArg q, TensorArg k, const float* lse, int B, int S, int H,
-                             float sm_scale, float* mass, hipStream_t st) {
+                             float sm_scale, KeyScale ks, float* mass, hipStream_t st) {
   const int n = blocks_of(S);
   const dim3 grid(n, H, B), block(128);
   if (dt == CHORUS_BF16)
-    hipLaunchKernelGGL(block_mass_kernel<true>, grid, block, 0, st, q, k, lse, S, H, n, sm_scale, mass);
+    hipLaunchKernelGGL(block_mass_kernel<true>, grid, block, 0, st, q, k, lse, S, H, n, sm_scale, ks, mass);
   else
-    hipLaunchKernelGGL(block_mass_kernel<false>, grid, block, 0, st, q, k, lse, S, H, n, sm_scale, mass);
+    hipLaunchKernelGGL(block_mass_kernel<false>, grid, block, 0, st, q, k, lse, S, H, n, sm_scale, ks, mass);
   return hipGetLastError();
 }
 

@@ -42,6 +42,13 @@ struct TensorArg {
   int64_t sb, ss, sh;
 };
 
+// First-frame key enhancement: keys of tokens < n_first count beta times
+// (n_first == 0: off).
+struct KeyScale {
+  int n_first;
+  float beta;
+};
+
 // ---- mask builder (mask_builder.hip) ----
 struct BuilderWorkspace {
   double* qbar;      // [B*H*n, D]
@@ -52,8 +59,8 @@ struct BuilderWorkspace {
   int32_t words;
 };
 BuilderWorkspace carve_builder(void* ws, int B, int H, int n, size_t* bytes);
-hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, double* qbar,
-                       double* kbar, hipStream_t st);
+hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, KeyScale ks,
+                       double* qbar, double* kbar, hipStream_t st);
 hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n,
                                double sm_scale, double top_p, int k_min, double* scores,
                                int32_t* counts, uint32_t* bitmap, int words, float* block_scores,
@@ -70,7 +77,7 @@ hipError_t launch_validate(const int32_t* row_ptr, const int32_t* col_idx, int64
 
 // ---- block mass and coverage (block_mass.hip) ----
 hipError_t launch_block_mass(chorus_dtype dt, TensorArg q, TensorArg k, const float* lse, int B, int S, int H,
-                             float sm_scale, float* mass, hipStream_t st);
+                             float sm_scale, KeyScale ks, float* mass, hipStream_t st);
 hipError_t launch_coverage(const int32_t* row_ptr, const int32_t* col_idx, int mask_batch, const float* mass, int B,
                            int S, int H, double* coverage, hipStream_t st);
 
@@ -98,6 +105,7 @@ struct AttnArgs {
   int B, S, H, n;
   int mask_batch;
   float sm_scale;
+  KeyScale ks;
 };
 hipError_t launch_attn_fwd_16(chorus_dtype dt, const AttnArgs& a, hipStream_t st);
 hipError_t launch_attn_fwd_fp8(const AttnArgs& a, hipStream_t st);

@@ -26,7 +26,8 @@ __device__ inline float to_f32(uint16_t bits, bool is_bf16) {
 // 16-byte column chunks; float64 partial sums, reduced over g by shuffles.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int S, int H, int n, bool bf16,
-                                                   double* __restrict__ qbar, double* __restrict__ kbar) {
+                                                   KeyScale ks, double* __restrict__ qbar,
+                                                   double* __restrict__ kbar) {
   const int blk = blockIdx.x, h = blockIdx.y;
   const int b = blockIdx.z >> 1, which = blockIdx.z & 1;
   const TensorArg t = which ? k : q;
@@ -39,13 +40,18 @@ __global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int 
   double acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+  // first-frame keys (Eq. 1) enter the sum beta times; otherwise weight 1,
+  // for which the fma is the plain sum
+  const int n_scaled = which ? ks.n_first : 0;
+  const double beta = (double)ks.beta;
   for (int tok = g; tok < cnt; tok += 4) {
     const uint4 raw = *reinterpret_cast<const uint4*>(base + (int64_t)(t0 + tok) * t.ss);
     const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+    const double wt = t0 + tok < n_scaled ? beta : 1.0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      acc[2 * e] += (double)to_f32(uint16_t(w[e] & 0xffff), bf16);
-      acc[2 * e + 1] += (double)to_f32(uint16_t(w[e] >> 16), bf16);
+      acc[2 * e] = __builtin_fma(wt, (double)to_f32(uint16_t(w[e] & 0xffff), bf16), acc[2 * e]);
+      acc[2 * e + 1] = __builtin_fma(wt, (double)to_f32(uint16_t(w[e] >> 16), bf16), acc[2 * e + 1]);
     }
   }
 #pragma unroll
@@ -855,11 +861,11 @@ __global__ __launch_bounds__(256) void validate_kernel(const int32_t* __restrict
 
 }  // namespace
 
-hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, double* qbar,
-                       double* kbar, hipStream_t st) {
+hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, KeyScale ks,
+                       double* qbar, double* kbar, hipStream_t st) {
   const int n = blocks_of(S);
-  hipLaunchKernelGGL(pool_kernel, dim3(n, H, 2 * B), dim3(64), 0, st, q, k, S, H, n, dt == CHORUS_BF16, qbar,
-                     kbar);
+  hipLaunchKernelGGL(pool_kernel, dim3(n, H, 2 * B), dim3(64), 0, st, q, k, S, H, n, dt == CHORUS_BF16, ks,
+                     qbar, kbar);
   return hipGetLastError();
 }
 

@@ -46,6 +46,18 @@ class Schedule(ctypes.Structure):
     _fields_ = [("order", ctypes.c_void_p), ("n_units", ctypes.c_int32)]
 
 
+class KeyScale(ctypes.Structure):
+    _fields_ = [("n_first", ctypes.c_int32), ("beta", ctypes.c_float)]
+
+
+def _key_scale(key_scale):
+    """(n_first, beta) -> pointer to a chorus_key_scale, None -> NULL."""
+    if key_scale is None:
+        return None
+    n_first, beta = key_scale
+    return ctypes.byref(KeyScale(int(n_first), float(beta)))
+
+
 EXPORTS = [
     "chorus_build_block_mask_workspace_size", "chorus_build_block_mask",
     "chorus_plan_workspace_size", "chorus_plan_block_mask", "chorus_validate_block_mask",
@@ -75,26 +87,27 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_size_t)
     sig = {
         "chorus_build_block_mask_workspace_size": (SZ, [P(Shape)]),
-        "chorus_build_block_mask": (I32, [I32, P(Shape), P(Tensor), P(Tensor), F64, F64, F64, VP, VP,
-                                          I64, VP, VP, SZ, VP]),
+        "chorus_build_block_mask": (I32, [I32, P(Shape), P(Tensor), P(Tensor), F64, F64, F64,
+                                          P(KeyScale), VP, VP, I64, VP, VP, SZ, VP]),
         "chorus_plan_workspace_size": (SZ, [P(Shape), P(Mask)]),
         "chorus_plan_block_mask": (I32, [P(Shape), P(Mask), VP, VP, SZ, VP]),
         "chorus_validate_block_mask": (I32, [P(Mask), I64, VP, VP]),
         "chorus_quantize_fp8_blockwise": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, VP]),
         "chorus_attn_workspace_size": (SZ, [I32, P(Shape), P(Mask)]),
         "chorus_block_sparse_attn_fwd": (I32, [I32, P(Shape), P(Tensor), P(Tensor), P(Tensor), VP,
-                                               VP, VP, P(Mask), P(Schedule), F32, P(Tensor), VP,
-                                               VP, SZ, VP]),
+                                               VP, VP, P(Mask), P(Schedule), F32, P(KeyScale),
+                                               P(Tensor), VP, VP, SZ, VP]),
         "chorus_block_sparse_attn_fwd_f16": (I32, [P(Shape), P(Tensor), P(Tensor), P(Tensor),
-                                                   P(Mask), P(Schedule), F32, P(Tensor), VP, VP,
-                                                   SZ, VP]),
+                                                   P(Mask), P(Schedule), F32, P(KeyScale),
+                                                   P(Tensor), VP, VP, SZ, VP]),
         "chorus_block_sparse_attn_fwd_bf16": (I32, [P(Shape), P(Tensor), P(Tensor), P(Tensor),
-                                                    P(Mask), P(Schedule), F32, P(Tensor), VP, VP,
-                                                    SZ, VP]),
+                                                    P(Mask), P(Schedule), F32, P(KeyScale),
+                                                    P(Tensor), VP, VP, SZ, VP]),
         "chorus_block_sparse_attn_fwd_fp8": (I32, [P(Shape), P(Tensor), P(Tensor), P(Tensor), VP,
-                                                   VP, VP, P(Mask), P(Schedule), F32, P(Tensor),
-                                                   VP, VP, SZ, VP]),
-        "chorus_attn_block_mass": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, F32, VP, VP]),
+                                                   VP, VP, P(Mask), P(Schedule), F32, P(KeyScale),
+                                                   P(Tensor), VP, VP, SZ, VP]),
+        "chorus_attn_block_mass": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, F32, P(KeyScale),
+                                         VP, VP]),
         "chorus_select_block_mask_workspace_size": (SZ, [P(Shape)]),
         "chorus_select_block_mask": (I32, [P(Shape), VP, F64, F64, VP, VP, I64, VP, SZ, VP]),
         "chorus_mask_coverage": (I32, [P(Shape), P(Mask), VP, VP, VP]),
@@ -211,8 +224,10 @@ class BlockMask:
 
 def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: float,
                      sm_scale: float | None = None, return_scores: bool = False,
-                     out: BlockMask | None = None, workspace: torch.Tensor | None = None) -> BlockMask:
-    """chorus_build_block_mask: one mask per request of ``q, k [B, S, H, D]``."""
+                     out: BlockMask | None = None, workspace: torch.Tensor | None = None,
+                     key_scale=None) -> BlockMask:
+    """chorus_build_block_mask: one mask per request of ``q, k [B, S, H, D]``;
+    ``key_scale = (n_first, beta)`` pools the first-frame-enhanced keys."""
     L = load_library()
     if q.shape != k.shape or q.dtype != k.dtype:
         raise ValueError("q and k must share shape and dtype")
@@ -231,7 +246,8 @@ def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: 
         workspace = _workspace(need, q.device)
     st = L.chorus_build_block_mask(
         _dtype_code(q), ctypes.byref(shape), ctypes.byref(_tensor(q)), ctypes.byref(_tensor(k)),
-        sm, float(top_p), float(min_top_k), out.row_ptr.data_ptr(), out.col_idx.data_ptr(),
+        sm, float(top_p), float(min_top_k), _key_scale(key_scale), out.row_ptr.data_ptr(),
+        out.col_idx.data_ptr(),
         out.col_idx.numel(), _ptr(out.block_scores if return_scores else None),
         _aligned(workspace), need, _stream())
     _check(st, "chorus_build_block_mask")
@@ -286,11 +302,12 @@ def quantize_fp8_blockwise(x: torch.Tensor, codes: torch.Tensor | None = None,
 
 def block_sparse_attn_fwd(q, k, v, mask: BlockMask | None, sm_scale: float | None = None,
                           scales=None, out: torch.Tensor | None = None, return_lse: bool = False,
-                          schedule: torch.Tensor | None = None):
+                          schedule: torch.Tensor | None = None, key_scale=None):
     """chorus_block_sparse_attn_fwd (dtype taken from q: f16, bf16 or uint8 fp8 codes).
 
     ``scales`` = (q_scale, k_scale, v_scale) for fp8 codes; ``mask=None`` runs
-    every block pair (dense attention).  Returns ``out`` (and ``lse [B, H, S]``
+    every block pair (dense attention); ``key_scale = (n_first, beta)`` applies
+    the first-frame key enhancement.  Returns ``out`` (and ``lse [B, H, S]``
     fp32 when ``return_lse``).
     """
     L = load_library()
@@ -315,7 +332,8 @@ def block_sparse_attn_fwd(q, k, v, mask: BlockMask | None, sm_scale: float | Non
     ws = _workspace(need, q.device)
     st = L.chorus_block_sparse_attn_fwd(dt, ctypes.byref(shape), ctypes.byref(_tensor(q)),
                                         ctypes.byref(_tensor(k)), ctypes.byref(_tensor(v)), qs, ks,
-                                        vs, cm, sched, sm, ctypes.byref(_tensor(out)),
+                                        vs, cm, sched, sm, _key_scale(key_scale),
+                                        ctypes.byref(_tensor(out)),
                                         _ptr(lse), _aligned(ws), need, _stream())
     _check(st, "chorus_block_sparse_attn_fwd")
     return (out, lse) if return_lse else out
@@ -337,9 +355,10 @@ def block_sparse_attn_fwd_fp8(q, k, v, q_scale, k_scale, v_scale, mask, **kw):
 
 
 def attn_block_mass(q: torch.Tensor, k: torch.Tensor, lse: torch.Tensor, sm_scale: float | None = None,
-                    out: torch.Tensor | None = None) -> torch.Tensor:
+                    out: torch.Tensor | None = None, key_scale=None) -> torch.Tensor:
     """chorus_attn_block_mass: true block attention mass [B, H, n, n] (fp32)
-    of ``q, k [B, S, H, D]`` given the dense attention's ``lse [B, H, S]``."""
+    of ``q, k [B, S, H, D]`` given the dense attention's ``lse [B, H, S]``
+    (computed with the same ``key_scale``)."""
     L = load_library()
     if q.shape != k.shape or q.dtype != k.dtype:
         raise ValueError("q and k must share shape and dtype")
@@ -352,7 +371,8 @@ def attn_block_mass(q: torch.Tensor, k: torch.Tensor, lse: torch.Tensor, sm_scal
     if mass.shape != (B, H, n, n) or mass.dtype != torch.float32 or not mass.is_contiguous():
         raise ValueError("out must be a contiguous float32 [B, H, n, n] tensor")
     st = L.chorus_attn_block_mass(_dtype_code(q), ctypes.byref(_shape(q)), ctypes.byref(_tensor(q)),
-                                  ctypes.byref(_tensor(k)), lse.data_ptr(), sm, mass.data_ptr(), _stream())
+                                  ctypes.byref(_tensor(k)), lse.data_ptr(), sm, _key_scale(key_scale),
+                                  mass.data_ptr(), _stream())
     _check(st, "chorus_attn_block_mass")
     return mass
 

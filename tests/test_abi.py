@@ -50,7 +50,7 @@ def shape(B=1, S=100, H=2, D=128):
     return ops.Shape(B, S, H, D)
 
 
-def build(lib, shp, q=None, top_p=0.5, mk=0.1, cap=None, ws_bytes=None, dtype=ops.BF16):
+def build(lib, shp, q=None, top_p=0.5, mk=0.1, cap=None, ws_bytes=None, dtype=ops.BF16, ks=None):
     n = (shp.S + 63) // 64
     rows = shp.B * shp.H * n
     cap = rows * n if cap is None else cap
@@ -58,7 +58,7 @@ def build(lib, shp, q=None, top_p=0.5, mk=0.1, cap=None, ws_bytes=None, dtype=op
     ws = need if ws_bytes is None else ws_bytes
     qq = q or t4(shp.B, shp.S, shp.H)
     return lib.chorus_build_block_mask(dtype, ctypes.byref(shp), ctypes.byref(qq), ctypes.byref(qq),
-                                       0.088, top_p, mk, FAKE, FAKE, cap, None, FAKE, ws, None)
+                                       0.088, top_p, mk, ks, FAKE, FAKE, cap, None, FAKE, ws, None)
 
 
 def test_builder_argument_checks(lib):
@@ -78,11 +78,11 @@ def test_builder_argument_checks(lib):
     assert b"stride" in lib.chorus_last_error()
 
 
-def attn(lib, shp, mask, dtype=ops.BF16, scales=(None, None, None), sched=None, sm=0.088):
+def attn(lib, shp, mask, dtype=ops.BF16, scales=(None, None, None), sched=None, sm=0.088, ks=None):
     t = t4(shp.B, shp.S, shp.H)
     return lib.chorus_block_sparse_attn_fwd(dtype, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
                                             ctypes.byref(t), *scales, ctypes.byref(mask),
-                                            sched, sm, ctypes.byref(t), None, None, 0, None)
+                                            sched, sm, ks, ctypes.byref(t), None, None, 0, None)
 
 
 def test_attention_argument_checks(lib):
@@ -119,13 +119,13 @@ def test_block_mass_selection_and_coverage_check_arguments(lib):
     shp = shape(B=1, S=100, H=2)
     t = t4()
     assert lib.chorus_attn_block_mass(ops.FP8_E4M3, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
-                                      FAKE, 0.088, FAKE, None) == 2
+                                      FAKE, 0.088, None, FAKE, None) == 2
     assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
-                                      None, 0.088, FAKE, None) == 1
+                                      None, 0.088, None, FAKE, None) == 1
     assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
-                                      FAKE, -1.0, FAKE, None) == 1
+                                      FAKE, -1.0, None, FAKE, None) == 1
     assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shape(D=64)), ctypes.byref(t), ctypes.byref(t),
-                                      FAKE, 0.088, FAKE, None) == 2
+                                      FAKE, 0.088, None, FAKE, None) == 2
     need = lib.chorus_select_block_mask_workspace_size(ctypes.byref(shp))
     assert need > 0
     sel = lib.chorus_select_block_mask
@@ -156,3 +156,19 @@ def test_visit_refresh_checks_arguments(lib):
     assert lib.chorus_visit_refresh(ctypes.byref(m), FAKE, FAKE, FAKE, 2 * 10 * 10 - 1, FAKE, need, None) == 3
     assert lib.chorus_visit_refresh(ctypes.byref(m), FAKE, FAKE, FAKE, 2 * 10 * 10, FAKE, need - 4, None) == 5
     assert lib.chorus_visit_refresh(ctypes.byref(m), None, FAKE, FAKE, 2 * 10 * 10, FAKE, need, None) == 1
+
+
+def test_key_scale_checks(lib):
+    shp = shape(B=2, S=100, H=2)
+    ok = ops.Mask(1, 2, 2, 64, FAKE, FAKE)
+    bad_n = ctypes.byref(ops.KeyScale(101, 2.0))
+    neg_n = ctypes.byref(ops.KeyScale(-1, 2.0))
+    nan_b = ctypes.byref(ops.KeyScale(10, float("nan")))
+    inf_b = ctypes.byref(ops.KeyScale(10, float("inf")))
+    for ks in (bad_n, neg_n, nan_b, inf_b):
+        assert attn(lib, shp, ok, ks=ks) == 1
+        assert build(lib, shape(), ks=ks) == 1
+        t = t4()
+        assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shape(B=1, S=100, H=2)), ctypes.byref(t),
+                                          ctypes.byref(t), FAKE, 0.088, ks, FAKE, None) == 1
+    assert b"key_scale" in lib.chorus_last_error()
