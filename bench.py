@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--f16", action="store_true",
+                    help="run a 16-bit workload in f16 (its inputs converted) instead of bf16")
     ap.add_argument("--coverage", action="store_true",
                     help="instead of the throughput line, print the mask-coverage study (true block-mass "
                          "masks of a historical request reused on similar requests)")
@@ -242,8 +244,16 @@ def main():
     ops.load_library()
     wl = wk.WORKLOADS[args.workload]
     inp = wk.make_inputs(wl)
-    q, k, v = inp.q.cuda(), inp.k.cuda(), inp.v.cuda()
     fp8 = wl.dtype == "fp8"
+    if args.f16:
+        if fp8:
+            sys.exit("--f16 applies to the 16-bit workloads only")
+        for name in ("q", "k", "v", "mask_q", "mask_k"):
+            x = getattr(inp, name, None)
+            if x is not None:
+                setattr(inp, name, x.to(torch.float16))
+    dtype_name = "f16" if args.f16 else wl.dtype
+    q, k, v = inp.q.cuda(), inp.k.cuda(), inp.v.cuda()
     B, S, H = wl.B, wl.S, wl.H
     n = wl.n_blocks
 
@@ -339,6 +349,15 @@ def main():
     build_ms = event_ms(build, reps) if mq is not None else 0.0
     plan_ms = event_ms(lambda: plan(mask), reps)
     quant_ms = event_ms(quant, reps) if fp8 else 0.0
+    build_fp8_ms = None
+    if fp8 and mq is not None:
+        # the builder reading fp8 codes of the mask source instead of 16-bit values
+        (mqc, mqs), (mkc, mks) = (ops.quantize_fp8_blockwise(x) for x in (mq, mk))
+        build_fp8_ms = event_ms(lambda: ops.build_block_mask(
+            mqc, mkc, wl.top_p, wl.min_top_k, sm_scale=wl.sm_scale, scales=(mqs, mks),
+            out=mask_buf, workspace=ws_build), reps)
+        del mqc, mqs, mkc, mks
+        build()                       # the step's own mask again
     # block-pair visit refreshing of a layer group (outside the step: one
     # update per layer, one refresh at the group's last layer).  The refresh
     # is timed in its worst case: the map holds only this mask's own pairs,
@@ -360,7 +379,7 @@ def main():
 
     kernel_file = "attn_fwd_fp8.hip" if fp8 else "attn_fwd.hip"
     src_hash = source_hash([kernel_file, "attn_common.h"])
-    traffic = traffic_from_profile(kernel_file, wl.key, src_hash)
+    traffic = traffic_from_profile(kernel_file, wl.key + ("_f16" if args.f16 else ""), src_hash)
 
     line = {
         "metric": "effective TFLOP/s on computed blocks & % MFMA peak; speedup vs 100%-density",
@@ -373,7 +392,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": wl.dtype,
+        "dtype": dtype_name,
         "data": "synthetic (seeded Wan-class Q/K/V on the latent grid; no real latents)",
         "config": {
             "workload": wl.key, "B": B, "S": S, "H": H, "D": 128, "block": 64,
@@ -387,6 +406,7 @@ def main():
         "attn_frac_mfma_peak": round(attn_tflops / peak, 4),
         "attn_key_scaled_ms": round(attn_ks_ms, 4),
         "builder_ms": round(build_ms, 4),
+        "builder_fp8_input_ms": None if build_fp8_ms is None else round(build_fp8_ms, 4),
         "plan_ms": round(plan_ms, 4),
         "quant_ms": round(quant_ms, 4),
         "visit_update_ms": round(visit_update_ms, 4),
@@ -396,7 +416,8 @@ def main():
         "speedup_vs_dense": round(dense_ms / attn_ms, 3),
         "ideal_speedup": round(float(mask.rows * n) / nnz, 3),
         "roofline": {
-            "kernel": ("attn_fwd_fp8_kernel<false>" if fp8 else "attn_fwd_16_kernel<true,false>"),
+            "kernel": ("attn_fwd_fp8_kernel<false, false>" if fp8 else
+                   f"attn_fwd_16_kernel<{'false' if args.f16 else 'true'}, false, false>"),
             "bound": "mfma",
             "achieved": round(attn_tflops, 2),
             "peak": peak,

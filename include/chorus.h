@@ -158,6 +158,20 @@ chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* sh
                                       float* block_scores, void* workspace,
                                       size_t workspace_bytes, void* stream);
 
+/* The builder on fp8 input: q, k are e4m3fn codes [B, S, H, D] (uint8, strides
+ * in bytes) with the fp32 block scales [B, H, n_blocks] of the quantiser;
+ * step 1 pools the values code * scale (the block's scale is constant, so
+ * the mean is scale * mean(code), in float64).  Everything else as
+ * chorus_build_block_mask (same workspace size).  dtype CHORUS_FP8_E4M3 on
+ * chorus_build_block_mask itself returns CHORUS_ERR_UNSUPPORTED. */
+chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const chorus_tensor* q,
+                                          const float* q_scale, const chorus_tensor* k,
+                                          const float* k_scale, double sm_scale, double top_p,
+                                          double min_top_k, const chorus_key_scale* key_scale,
+                                          int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                          float* block_scores, void* workspace,
+                                          size_t workspace_bytes, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Work plan -- the one-GPU counterpart of the paper's head-level scheduling
  * (Sec. 3.2 "Head-level scheduling for load balancing", Appendix A): because

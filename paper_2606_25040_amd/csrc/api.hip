@@ -144,20 +144,21 @@ size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape) {
   return bytes;
 }
 
-chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
-                                      const chorus_tensor* q, const chorus_tensor* k,
-                                      double sm_scale, double top_p, double min_top_k,
-                                      const chorus_key_scale* key_scale,
-                                      int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
-                                      float* block_scores, void* workspace,
-                                      size_t workspace_bytes, void* stream) {
+static chorus_status build_mask_impl(chorus_dtype dtype, const chorus_shape* shape, const chorus_tensor* q,
+                                     const float* q_scale, const chorus_tensor* k, const float* k_scale,
+                                     double sm_scale, double top_p, double min_top_k,
+                                     const chorus_key_scale* key_scale, int32_t* row_ptr, int32_t* col_idx,
+                                     int64_t col_capacity, float* block_scores, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
   g_last_error[0] = 0;
   chorus_status st;
   if ((st = check_shape(shape))) return st;
-  if (dtype != CHORUS_F16 && dtype != CHORUS_BF16)
-    return fail(CHORUS_ERR_UNSUPPORTED, "builder input dtype %d unsupported (f16/bf16)", (int)dtype);
-  if ((st = check_tensor(q, "q", 2))) return st;
-  if ((st = check_tensor(k, "k", 2))) return st;
+  const bool fp8 = dtype == CHORUS_FP8_E4M3;
+  if (dtype != CHORUS_F16 && dtype != CHORUS_BF16 && !fp8)
+    return fail(CHORUS_ERR_UNSUPPORTED, "builder input dtype %d unsupported (f16/bf16/fp8)", (int)dtype);
+  if ((st = check_tensor(q, "q", fp8 ? 1 : 2))) return st;
+  if ((st = check_tensor(k, "k", fp8 ? 1 : 2))) return st;
+  if (fp8 && (!q_scale || !k_scale)) return fail(CHORUS_ERR_INVALID_ARG, "fp8 input needs q_scale and k_scale");
   const int n = blocks_of(shape->S);
   if (n > kMaxBuilderBlocks)
     return fail(CHORUS_ERR_UNSUPPORTED, "n_blocks=%d exceeds builder limit %d", n, kMaxBuilderBlocks);
@@ -179,15 +180,41 @@ chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* sh
   if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
   const int k_min = (int)std::ceil(min_top_k * (double)n - 1e-9);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = from_hip(launch_pool(dtype, targ(q), targ(k), shape->B, shape->S, shape->H, ks, w.qbar, w.kbar, s),
-                     "pool")))
-    return st;
+  const hipError_t pe =
+      fp8 ? launch_pool_fp8(targ(q), q_scale, targ(k), k_scale, shape->B, shape->S, shape->H, ks, w.qbar, w.kbar, s)
+          : launch_pool(dtype, targ(q), targ(k), shape->B, shape->S, shape->H, ks, w.qbar, w.kbar, s);
+  if ((st = from_hip(pe, "pool"))) return st;
   if ((st = from_hip(launch_score_select(w.qbar, w.kbar, shape->B, shape->H, n, sm_scale, top_p,
                                          k_min, w.scores, w.counts, w.bitmap, w.words, block_scores, s),
                      "score_select")))
     return st;
   if ((st = from_hip(launch_scan_counts(w.counts, rows, row_ptr, s), "scan"))) return st;
   return from_hip(launch_compact(w.bitmap, w.words, row_ptr, rows, col_idx, s), "compact");
+}
+
+chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
+                                      const chorus_tensor* q, const chorus_tensor* k,
+                                      double sm_scale, double top_p, double min_top_k,
+                                      const chorus_key_scale* key_scale,
+                                      int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                      float* block_scores, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  if (dtype == CHORUS_FP8_E4M3) {
+    g_last_error[0] = 0;
+    return fail(CHORUS_ERR_UNSUPPORTED, "fp8 input goes through chorus_build_block_mask_fp8 (it needs scales)");
+  }
+  return build_mask_impl(dtype, shape, q, nullptr, k, nullptr, sm_scale, top_p, min_top_k, key_scale, row_ptr,
+                         col_idx, col_capacity, block_scores, workspace, workspace_bytes, stream);
+}
+
+chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const chorus_tensor* q, const float* q_scale,
+                                          const chorus_tensor* k, const float* k_scale, double sm_scale,
+                                          double top_p, double min_top_k, const chorus_key_scale* key_scale,
+                                          int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                          float* block_scores, void* workspace, size_t workspace_bytes,
+                                          void* stream) {
+  return build_mask_impl(CHORUS_FP8_E4M3, shape, q, q_scale, k, k_scale, sm_scale, top_p, min_top_k, key_scale,
+                         row_ptr, col_idx, col_capacity, block_scores, workspace, workspace_bytes, stream);
 }
 
 size_t chorus_plan_workspace_size(const chorus_shape* shape, const chorus_block_mask* mask) {

@@ -61,6 +61,8 @@ struct BuilderWorkspace {
 BuilderWorkspace carve_builder(void* ws, int B, int H, int n, size_t* bytes);
 hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, KeyScale ks,
                        double* qbar, double* kbar, hipStream_t st);
+hipError_t launch_pool_fp8(TensorArg q, const float* q_scale, TensorArg k, const float* k_scale, int B, int S,
+                           int H, KeyScale ks, double* qbar, double* kbar, hipStream_t st);
 hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n,
                                double sm_scale, double top_p, int k_min, double* scores,
                                int32_t* counts, uint32_t* bitmap, int words, float* block_scores,

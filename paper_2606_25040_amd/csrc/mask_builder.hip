@@ -66,6 +66,60 @@ __global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int 
   }
 }
 
+// OCP e4m3fn code -> float, exactly: bias 7, three mantissa bits, subnormals
+// m * 2^-9, S.1111.111 is NaN, no infinities.
+__device__ inline float e4m3_to_f32(uint32_t c) {
+  const uint32_t e = (c >> 3) & 15u, m = c & 7u;
+  float mag = e == 0 ? (float)m * 0x1p-9f : __uint_as_float(((e + 120u) << 23) | (m << 20));
+  if (e == 15u && m == 7u) mag = __builtin_nanf("");
+  return (c & 0x80u) ? -mag : mag;
+}
+
+// 1b. Block mean-pool of fp8 e4m3 codes with per-(request, head, block)
+// scales, as written by the fp8 quantiser: the mean of code * scale over the
+// block's valid tokens, summed over codes in float64 and scaled once.  Same
+// lane layout as pool_kernel, eight codes (8 bytes) per lane and token.
+__global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* __restrict__ q_scale, TensorArg k,
+                                                      const float* __restrict__ k_scale, int S, int H, int n,
+                                                      KeyScale ks, double* __restrict__ qbar,
+                                                      double* __restrict__ kbar) {
+  const int blk = blockIdx.x, h = blockIdx.y;
+  const int b = blockIdx.z >> 1, which = blockIdx.z & 1;
+  const TensorArg t = which ? k : q;
+  const float* sc = which ? k_scale : q_scale;
+  double* out = which ? kbar : qbar;
+  const int lane = threadIdx.x;
+  const int g = lane >> 4, c = lane & 15;
+  const int t0 = blk * kBlock;
+  const int cnt = min(kBlock, S - t0);
+  const uint8_t* base = static_cast<const uint8_t*>(t.data) + (int64_t)b * t.sb + (int64_t)h * t.sh + c * 8;
+  double acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+  const int n_scaled = which ? ks.n_first : 0;
+  const double beta = (double)ks.beta;
+  for (int tok = g; tok < cnt; tok += 4) {
+    const uint2 raw = *reinterpret_cast<const uint2*>(base + (int64_t)(t0 + tok) * t.ss);
+    const double wt = t0 + tok < n_scaled ? beta : 1.0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t word = e < 4 ? raw.x : raw.y;
+      acc[e] = __builtin_fma(wt, (double)e4m3_to_f32((word >> (8 * (e & 3))) & 0xffu), acc[e]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    acc[e] += __shfl_xor(acc[e], 16);
+    acc[e] += __shfl_xor(acc[e], 32);
+  }
+  if (g == 0) {
+    const double scale = (double)sc[((int64_t)b * H + h) * n + blk];
+    double* dst = out + ((int64_t)(b * H + h) * n + blk) * kHeadDim + c * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dst[e] = acc[e] * scale / (double)cnt;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // 2a. Block scores s = sm_scale * qbar kbar^T per (request, head): a float64
 // GEMM tile of 128 x 128 outputs per workgroup of 256 threads (8 x 8 outputs
@@ -860,6 +914,14 @@ __global__ __launch_bounds__(256) void validate_kernel(const int32_t* __restrict
 }
 
 }  // namespace
+
+hipError_t launch_pool_fp8(TensorArg q, const float* q_scale, TensorArg k, const float* k_scale, int B, int S,
+                           int H, KeyScale ks, double* qbar, double* kbar, hipStream_t st) {
+  const int n = blocks_of(S);
+  hipLaunchKernelGGL(pool_fp8_kernel, dim3(n, H, 2 * B), dim3(64), 0, st, q, q_scale, k, k_scale, S, H, n, ks, qbar,
+                     kbar);
+  return hipGetLastError();
+}
 
 hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, KeyScale ks,
                        double* qbar, double* kbar, hipStream_t st) {

@@ -59,7 +59,7 @@ def _key_scale(key_scale):
 
 
 EXPORTS = [
-    "chorus_build_block_mask_workspace_size", "chorus_build_block_mask",
+    "chorus_build_block_mask_workspace_size", "chorus_build_block_mask", "chorus_build_block_mask_fp8",
     "chorus_plan_workspace_size", "chorus_plan_block_mask", "chorus_validate_block_mask",
     "chorus_quantize_fp8_blockwise", "chorus_attn_workspace_size",
     "chorus_block_sparse_attn_fwd", "chorus_block_sparse_attn_fwd_f16",
@@ -89,6 +89,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "chorus_build_block_mask_workspace_size": (SZ, [P(Shape)]),
         "chorus_build_block_mask": (I32, [I32, P(Shape), P(Tensor), P(Tensor), F64, F64, F64,
                                           P(KeyScale), VP, VP, I64, VP, VP, SZ, VP]),
+        "chorus_build_block_mask_fp8": (I32, [P(Shape), P(Tensor), VP, P(Tensor), VP, F64, F64, F64,
+                                              P(KeyScale), VP, VP, I64, VP, VP, SZ, VP]),
         "chorus_plan_workspace_size": (SZ, [P(Shape), P(Mask)]),
         "chorus_plan_block_mask": (I32, [P(Shape), P(Mask), VP, VP, SZ, VP]),
         "chorus_validate_block_mask": (I32, [P(Mask), I64, VP, VP]),
@@ -225,12 +227,17 @@ class BlockMask:
 def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: float,
                      sm_scale: float | None = None, return_scores: bool = False,
                      out: BlockMask | None = None, workspace: torch.Tensor | None = None,
-                     key_scale=None) -> BlockMask:
+                     key_scale=None, scales=None) -> BlockMask:
     """chorus_build_block_mask: one mask per request of ``q, k [B, S, H, D]``;
-    ``key_scale = (n_first, beta)`` pools the first-frame-enhanced keys."""
+    ``key_scale = (n_first, beta)`` pools the first-frame-enhanced keys.  For
+    fp8 codes (uint8) pass ``scales = (q_scale, k_scale)`` from the quantiser
+    (chorus_build_block_mask_fp8)."""
     L = load_library()
     if q.shape != k.shape or q.dtype != k.dtype:
         raise ValueError("q and k must share shape and dtype")
+    fp8 = q.dtype == torch.uint8
+    if fp8 != (scales is not None):
+        raise ValueError("scales are given exactly for fp8 codes")
     B, S, H, D = q.shape
     n = (S + BLOCK - 1) // BLOCK
     rows = B * H * n
@@ -244,13 +251,18 @@ def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: 
     need = L.chorus_build_block_mask_workspace_size(ctypes.byref(shape))
     if workspace is None or workspace.numel() < need + 256:
         workspace = _workspace(need, q.device)
-    st = L.chorus_build_block_mask(
-        _dtype_code(q), ctypes.byref(shape), ctypes.byref(_tensor(q)), ctypes.byref(_tensor(k)),
-        sm, float(top_p), float(min_top_k), _key_scale(key_scale), out.row_ptr.data_ptr(),
-        out.col_idx.data_ptr(),
-        out.col_idx.numel(), _ptr(out.block_scores if return_scores else None),
-        _aligned(workspace), need, _stream())
-    _check(st, "chorus_build_block_mask")
+    tail = (sm, float(top_p), float(min_top_k), _key_scale(key_scale), out.row_ptr.data_ptr(),
+            out.col_idx.data_ptr(), out.col_idx.numel(),
+            _ptr(out.block_scores if return_scores else None), _aligned(workspace), need, _stream())
+    if fp8:
+        st = L.chorus_build_block_mask_fp8(ctypes.byref(shape), ctypes.byref(_tensor(q)),
+                                           scales[0].data_ptr(), ctypes.byref(_tensor(k)),
+                                           scales[1].data_ptr(), *tail)
+        _check(st, "chorus_build_block_mask_fp8")
+    else:
+        st = L.chorus_build_block_mask(_dtype_code(q), ctypes.byref(shape), ctypes.byref(_tensor(q)),
+                                       ctypes.byref(_tensor(k)), *tail)
+        _check(st, "chorus_build_block_mask")
     return out
 
 

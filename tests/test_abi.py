@@ -172,3 +172,20 @@ def test_key_scale_checks(lib):
         assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shape(B=1, S=100, H=2)), ctypes.byref(t),
                                           ctypes.byref(t), FAKE, 0.088, ks, FAKE, None) == 1
     assert b"key_scale" in lib.chorus_last_error()
+
+
+def test_fp8_builder_checks_arguments(lib):
+    shp = shape()
+    n = (shp.S + 63) // 64
+    cap = shp.B * shp.H * n * n
+    need = lib.chorus_build_block_mask_workspace_size(ctypes.byref(shp))
+    t8 = ops.Tensor(FAKE, 100 * 2 * 128, 2 * 128, 128)
+    f = lib.chorus_build_block_mask_fp8
+    assert f(ctypes.byref(shp), ctypes.byref(t8), None, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, None,
+             FAKE, FAKE, cap, None, FAKE, need, None) == 1
+    assert f(ctypes.byref(shp), ctypes.byref(t8), FAKE, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, None,
+             FAKE, FAKE, cap - 1, None, FAKE, need, None) == 3
+    assert f(ctypes.byref(shape(D=64)), ctypes.byref(t8), FAKE, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, None,
+             FAKE, FAKE, cap, None, FAKE, need, None) == 2
+    assert f(ctypes.byref(shp), ctypes.byref(ops.Tensor(FAKE + 4, 100 * 2 * 128, 2 * 128, 128)), FAKE,
+             ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, None, FAKE, FAKE, cap, None, FAKE, need, None) == 1

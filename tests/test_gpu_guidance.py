@@ -182,3 +182,4 @@ def test_full_size_720p_fp8_with_first_frame_enhancement():
             o_ref, _ = oa.attention_block(qh, kh, vh, oa.row_blocks(rp, ci, r), i, wl.sm_scale)
             worst = max(worst, max_abs_err(oh[i * 64:i * 64 + o_ref.shape[0]], o_ref))
     assert worst <= TOL8, worst
+
