@@ -69,13 +69,15 @@ def _softmax_rows(z: np.ndarray, v: np.ndarray):
 
 
 def attention_block(qh, kh, vh, kv_blocks, i: int, sm_scale: float,
-                    block: int = BLOCK, form: str = "gather"):
+                    block: int = BLOCK, form: str = "gather", kv_block: int | None = None):
     """Output rows of q-block ``i`` for one (batch, head).
 
     qh, kh, vh: ``[S, D]`` arrays holding the exact values the kernel reads.
-    kv_blocks: the kv-block ids listed for this mask row (any order).
+    kv_blocks: the kv-block ids listed for this mask row (any order), in
+    units of ``kv_block`` tokens (default ``block``; q-blocks are ``block``).
     Returns ``(O_i [rows, D], lse_i [rows])`` in float64, rows = valid queries.
     """
+    kvb = block if kv_block is None else kv_block
     qh = np.asarray(qh, dtype=np.float64)
     kh = np.asarray(kh, dtype=np.float64)
     vh = np.asarray(vh, dtype=np.float64)
@@ -85,11 +87,11 @@ def attention_block(qh, kh, vh, kv_blocks, i: int, sm_scale: float,
     if form == "literal":
         z = sm_scale * (qi @ kh.T)
         allowed = np.zeros(S, dtype=bool)
-        allowed[allowed_keys(kv_blocks, S, block)] = True
+        allowed[allowed_keys(kv_blocks, S, kvb)] = True
         z[:, ~allowed] = -np.inf
         return _softmax_rows(z, vh)
     if form == "gather":
-        idx = allowed_keys(sorted(set(int(j) for j in kv_blocks)), S, block)
+        idx = allowed_keys(sorted(set(int(j) for j in kv_blocks)), S, kvb)
         z = sm_scale * (qi @ kh[idx].T)
         return _softmax_rows(z, vh[idx])
     raise ValueError(f"unknown form {form!r}")
@@ -126,9 +128,11 @@ def row_blocks(row_ptr, col_idx, r: int) -> np.ndarray:
 
 
 def attention(q, k, v, row_ptr, col_idx, sm_scale: float, mask_batch: int = 1,
-              block: int = BLOCK, form: str = "gather"):
+              block: int = BLOCK, form: str = "gather", kv_block: int | None = None):
     """Full block-masked attention for ``[B, S, H, D]`` inputs.
 
+    Mask rows are q-blocks of ``block`` tokens, its ids kv blocks of
+    ``kv_block`` tokens (default ``block``).
     Returns ``O [B, S, H, D]`` and ``lse [B, H, S]`` (float64).
     """
     B, S, H, D = q.shape
@@ -145,7 +149,7 @@ def attention(q, k, v, row_ptr, col_idx, sm_scale: float, mask_batch: int = 1,
             for i in range(nb):
                 r = mask_row_index(b, h, i, H, nb, mask_batch)
                 o_i, l_i = attention_block(qh, kh, vh, row_blocks(row_ptr, col_idx, r), i,
-                                           sm_scale, block, form)
+                                           sm_scale, block, form, kv_block)
                 rows = slice(i * block, i * block + o_i.shape[0])
                 O[b, rows, h, :] = o_i
                 lse[b, h, rows] = l_i

@@ -101,38 +101,48 @@ class OracleMask:
     row_ptr: np.ndarray   # int64 [R + 1]
     col_idx: np.ndarray   # int64 [nnz]
     scores: np.ndarray    # float64 [R, n]
-    n_blocks: int
+    n_blocks: int          # q-blocks per head (rows per head)
     H: int
     mask_batch: int
+    n_kv: int = 0          # kv blocks per row (columns); 0 means n_blocks
 
     @property
     def nnz(self) -> int:
         return int(self.row_ptr[-1])
 
     @property
+    def columns(self) -> int:
+        return self.n_kv or self.n_blocks
+
+    @property
     def density(self) -> float:
         R = self.row_ptr.shape[0] - 1
-        return self.nnz / float(R * self.n_blocks)
+        return self.nnz / float(R * self.columns)
 
     def row(self, r: int) -> np.ndarray:
         return self.col_idx[self.row_ptr[r]:self.row_ptr[r + 1]]
 
 
 def build_block_mask(q, k, sm_scale: float, top_p: float, min_top_k: float,
-                     block: int = BLOCK, heads=None) -> OracleMask:
+                     block: int = BLOCK, heads=None, kv_block: int | None = None) -> OracleMask:
     """Steps 1-7 for every request b and head h of ``q, k [B, S, H, D]``.
 
-    ``heads`` optionally restricts the heads built (rows of other heads are
-    left empty); used to time a bounded sample.
+    Queries are pooled over blocks of ``block`` tokens (the mask's rows), keys
+    over blocks of ``kv_block`` tokens (its columns; default ``block``): the
+    paper's own kernel pairs q-blocks of 64 with kv blocks of 128.  ``heads``
+    optionally restricts the heads built (rows of other heads are left
+    empty); used to time a bounded sample.
     """
+    kvb = block if kv_block is None else kv_block
     B, S, H, D = q.shape
     n = (S + block - 1) // block
+    nk = (S + kvb - 1) // kvb
     counts = np.zeros(B * H * n, dtype=np.int64)
     rows = [None] * (B * H * n)
-    scores = np.zeros((B * H * n, n), dtype=np.float64)
+    scores = np.zeros((B * H * n, nk), dtype=np.float64)
     for b in range(B):
         for h in (range(H) if heads is None else heads):
-            s = block_scores(pool_means(q[b, :, h, :], block), pool_means(k[b, :, h, :], block),
+            s = block_scores(pool_means(q[b, :, h, :], block), pool_means(k[b, :, h, :], kvb),
                              sm_scale)
             for i in range(n):
                 r = (b * H + h) * n + i
@@ -144,4 +154,4 @@ def build_block_mask(q, k, sm_scale: float, top_p: float, min_top_k: float,
     np.cumsum(counts, out=row_ptr[1:])
     col_idx = np.concatenate([x for x in rows if x is not None]) if row_ptr[-1] else \
         np.zeros(0, np.int64)
-    return OracleMask(row_ptr, col_idx.astype(np.int64), scores, n, H, B)
+    return OracleMask(row_ptr, col_idx.astype(np.int64), scores, n, H, B, nk)

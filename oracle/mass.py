@@ -47,28 +47,33 @@ def attention_probs(qh, kh, sm_scale: float) -> np.ndarray:
     return e / e.sum(axis=1, keepdims=True)
 
 
-def block_mass(qh, kh, sm_scale: float, block: int = BLOCK) -> np.ndarray:
-    """M [n, n]: mean over the valid queries of q-block i of their attention
-    mass on the keys of block j."""
+def block_mass(qh, kh, sm_scale: float, block: int = BLOCK, kv_block: int | None = None) -> np.ndarray:
+    """M [n, n_kv]: mean over the valid queries of q-block i (``block``
+    tokens) of their attention mass on the keys of kv block j (``kv_block``
+    tokens, default ``block``)."""
+    kvb = block if kv_block is None else kv_block
     P = attention_probs(qh, kh, sm_scale)
     S = P.shape[0]
     n = (S + block - 1) // block
-    M = np.empty((n, n), dtype=np.float64)
+    nk = (S + kvb - 1) // kvb
+    M = np.empty((n, nk), dtype=np.float64)
     for i in range(n):
         rows = P[i * block:min(i * block + block, S)]
-        for j in range(n):
-            M[i, j] = rows[:, j * block:min(j * block + block, S)].sum() / rows.shape[0]
+        for j in range(nk):
+            M[i, j] = rows[:, j * kvb:min(j * kvb + kvb, S)].sum() / rows.shape[0]
     return M
 
 
-def block_mass_all(q, k, sm_scale: float, block: int = BLOCK) -> np.ndarray:
-    """M for every request and head of ``q, k [B, S, H, D]`` -> [B, H, n, n]."""
+def block_mass_all(q, k, sm_scale: float, block: int = BLOCK, kv_block: int | None = None) -> np.ndarray:
+    """M for every request and head of ``q, k [B, S, H, D]`` -> [B, H, n, n_kv]."""
+    kvb = block if kv_block is None else kv_block
     B, S, H, _ = q.shape
     n = (S + block - 1) // block
-    out = np.empty((B, H, n, n), dtype=np.float64)
+    nk = (S + kvb - 1) // kvb
+    out = np.empty((B, H, n, nk), dtype=np.float64)
     for b in range(B):
         for h in range(H):
-            out[b, h] = block_mass(q[b, :, h], k[b, :, h], sm_scale, block)
+            out[b, h] = block_mass(q[b, :, h], k[b, :, h], sm_scale, block, kvb)
     return out
 
 
@@ -86,7 +91,7 @@ def select_row_from_mass(m_row, top_p: float, min_top_k: float) -> np.ndarray:
 
 
 def mask_from_mass(M, top_p: float, min_top_k: float):
-    """CSR mask (mask_batch = B) from block masses ``M [B, H, n, n]``."""
+    """CSR mask (mask_batch = B) from block masses ``M [B, H, n, n_kv]``."""
     B, H, n, _ = M.shape
     rows = [select_row_from_mass(M[b, h, i], top_p, min_top_k)
             for b in range(B) for h in range(H) for i in range(n)]
@@ -105,7 +110,8 @@ def valid_counts(S: int, block: int = BLOCK) -> np.ndarray:
 
 def coverage(row_ptr, col_idx, mask_batch: int, M, S: int, block: int = BLOCK) -> np.ndarray:
     """Coverage [B, H] of a CSR mask on the requests whose block masses are
-    ``M [B, H, n, n]`` (row m = ((b if mask_batch > 1 else 0) * H + h) * n + i)."""
+    ``M [B, H, n, n_kv]`` (row m = ((b if mask_batch > 1 else 0) * H + h) * n + i;
+    ``block`` is the q-block size, the weights |T_i| are its valid tokens)."""
     B, H, n, _ = M.shape
     w = valid_counts(S, block)
     out = np.empty((B, H), dtype=np.float64)
