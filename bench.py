@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--kv-block", type=int, default=64, choices=(64, 128),
+                    help="tokens per kv block of the built mask (128 = the paper's kernel geometry)")
     ap.add_argument("--f16", action="store_true",
                     help="run a 16-bit workload in f16 (its inputs converted) instead of bf16")
     ap.add_argument("--coverage", action="store_true",
@@ -282,11 +284,15 @@ def main():
         codes = [torch.empty((B, S, H, 128), dtype=torch.uint8, device="cuda") for _ in range(3)]
         scales = [torch.empty((B, H, n), dtype=torch.float32, device="cuda") for _ in range(3)]
 
+    kvb = args.kv_block
+    if kvb != 64 and mq is None:
+        sys.exit("--kv-block 128 needs a workload whose mask is built")
+
     def build():
         if mq is None:
             return fixed
         return ops.build_block_mask(mq, mk, wl.top_p, wl.min_top_k, sm_scale=wl.sm_scale,
-                                    out=mask_buf, workspace=ws_build)
+                                    out=mask_buf, workspace=ws_build, kv_block=kvb)
 
     def plan(m):
         return ops.plan_block_mask(m, B, S, out=order, workspace=ws_plan)
@@ -325,7 +331,13 @@ def main():
     sched = plan(mask)
     torch.cuda.synchronize()
     nnz = mask.nnz
-    pairs = B * nnz
+    # computed 64 x 64 block pairs: a kv block of 128 is two, except a last
+    # block of 64 tokens or fewer (odd number of q-blocks)
+    sub = nnz
+    if kvb == 128:
+        _, ids = mask.to_host()
+        sub = 2 * nnz - (int((ids == mask.n_kv - 1).sum()) if n % 2 else 0)
+    pairs = B * sub
     flops = pairs * FLOP_PER_PAIR
     value = flops / (ms_per_step * 1e-3) / 1e12
 
@@ -362,11 +374,11 @@ def main():
     # update per layer, one refresh at the group's last layer).  The refresh
     # is timed in its worst case: the map holds only this mask's own pairs,
     # so every other pair is forced in and the output is dense.
-    vmap = ops.VisitMap(mask.mask_batch, H, n)
+    vmap = ops.VisitMap(mask.mask_batch, H, n, block=mask.block)
     vmap.reset(mask)
     refreshed = ops.BlockMask(torch.empty_like(mask.row_ptr),
-                              torch.empty(mask.rows * n, dtype=torch.int32, device="cuda"),
-                              mask.mask_batch, H, n)
+                              torch.empty(mask.rows * mask.n_kv, dtype=torch.int32, device="cuda"),
+                              mask.mask_batch, H, n, mask.block)
     need = ops.load_library().chorus_visit_refresh_workspace_size(ops.ctypes.byref(mask.as_c()))
     ws_visit = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
     visit_update_ms = event_ms(lambda: vmap.update(mask), reps)
@@ -379,7 +391,8 @@ def main():
 
     kernel_file = "attn_fwd_fp8.hip" if fp8 else "attn_fwd.hip"
     src_hash = source_hash([kernel_file, "attn_common.h"])
-    traffic = traffic_from_profile(kernel_file, wl.key + ("_f16" if args.f16 else ""), src_hash)
+    variant = ("_f16" if args.f16 else "") + ("_kv128" if kvb == 128 else "")
+    traffic = traffic_from_profile(kernel_file, wl.key + variant, src_hash)
 
     line = {
         "metric": "effective TFLOP/s on computed blocks & % MFMA peak; speedup vs 100%-density",
@@ -397,7 +410,8 @@ def main():
         "config": {
             "workload": wl.key, "B": B, "S": S, "H": H, "D": 128, "block": 64,
             "grid_tyx": list(wl.grid), "mask_source": wl.mask_source,
-            "target_density": wl.density, "density": round(nnz / float(mask.rows * n), 5),
+            "kv_block": kvb,
+            "target_density": wl.density, "density": round(sub / float(mask.rows * n), 5),
             "top_p": wl.top_p, "min_top_k": wl.min_top_k, "computed_pairs": pairs,
             "step": "mask build + plan" + (" + fp8 quantise" if fp8 else "") + " + attention",
         },
@@ -414,10 +428,11 @@ def main():
         "routing_overhead_ratio": round(build_ms / (build_ms + attn_ms), 4),
         "dense_attn_ms": round(dense_ms, 4),
         "speedup_vs_dense": round(dense_ms / attn_ms, 3),
-        "ideal_speedup": round(float(mask.rows * n) / nnz, 3),
+        "ideal_speedup": round(float(mask.rows * n) / sub, 3),
         "roofline": {
-            "kernel": ("attn_fwd_fp8_kernel<false, false>" if fp8 else
-                   f"attn_fwd_16_kernel<{'false' if args.f16 else 'true'}, false, false>"),
+            "kernel": (f"attn_fwd_fp8_kernel<false, false, {str(kvb == 128).lower()}>" if fp8 else
+                       f"attn_fwd_16_kernel<{str(not args.f16).lower()}, false, false, "
+                       f"{str(kvb == 128).lower()}>"),
             "bound": "mfma",
             "achieved": round(attn_tflops, 2),
             "peak": peak,

@@ -25,13 +25,15 @@
  *    H heads, head dim D contiguous (the layout the paper indexes as
  *    K[:, 0:N0, :, :] in Eq. (1)).  Strides are in elements; every token row
  *    (D elements) must start 16-byte aligned.  D must be 128.
- *  - Tokens are grouped in blocks of 64 (the mask granularity); n_blocks =
- *    ceil(S / 64).  A partial last block is handled inside the kernels (no
- *    padding is required in memory): keys at or beyond S carry no weight,
- *    output rows at or beyond S do not exist.
+ *  - Query tokens are grouped in blocks of 64 (the mask rows); n_blocks =
+ *    ceil(S / 64).  Key tokens are grouped in kv blocks of 64, or of 128 (the
+ *    paper's own kernel geometry, K block 128 with Q block 64, Sec. 4.1);
+ *    n_kv = ceil(S / kv_block).  A partial last block is handled inside the
+ *    kernels (no padding is required in memory): keys at or beyond S carry
+ *    no weight, output rows at or beyond S do not exist.
  *  - A block mask is CSR over rows r = (b_m * H + h) * n_blocks + i for mask
- *    request b_m, head h and query block i; row r lists the kv blocks that
- *    q-block i attends to, strictly ascending.  mask_batch == B gives one mask
+ *    request b_m, head h and query block i; row r lists the kv blocks (ids in
+ *    [0, n_kv)) that q-block i attends to, strictly ascending.  mask_batch == B gives one mask
  *    per request; mask_batch == 1 reuses one mask for every request (the
  *    cross-request reuse the paper is about).
  *  - Functions return chorus_status.  Arguments are validated on the host
@@ -53,7 +55,7 @@ extern "C" {
 typedef enum {
   CHORUS_OK = 0,
   CHORUS_ERR_INVALID_ARG = 1,  /* null pointer, bad shape/stride/alignment, bad knob   */
-  CHORUS_ERR_UNSUPPORTED = 2,  /* D != 128, block != 64, too many blocks, bad dtype    */
+  CHORUS_ERR_UNSUPPORTED = 2,  /* D != 128, kv block not 64/128, too many blocks, dtype */
   CHORUS_ERR_CAPACITY = 3,     /* col_idx capacity below the worst case               */
   CHORUS_ERR_HIP = 4,          /* a HIP launch or runtime call failed                 */
   CHORUS_ERR_WORKSPACE = 5     /* workspace missing or smaller than the queried size  */
@@ -85,8 +87,10 @@ typedef struct {
 typedef struct {
   int32_t mask_batch;       /* 1 or B                                           */
   int32_t H;                /* heads; must equal the shape's H                  */
-  int32_t n_blocks;         /* ceil(S / block); q-blocks = kv-blocks per head   */
-  int32_t block;            /* tokens per block; must be 64                     */
+  int32_t n_blocks;         /* ceil(S / 64): q-blocks (rows) per head           */
+  int32_t block;            /* tokens per kv block: 64 or 128; the ids of a row */
+                            /* lie in [0, n_kv), n_kv = ceil(n_blocks * 64 /    */
+                            /* block) = ceil(S / block)                         */
   const int32_t* row_ptr;   /* [mask_batch * H * n_blocks + 1], row_ptr[0] == 0 */
   const int32_t* col_idx;   /* [nnz] ascending kv-block ids per row             */
 } chorus_block_mask;
@@ -122,28 +126,30 @@ typedef struct {
  * "Minimum top-k guarantee", Sec. 4.1 (top_p, min_top_k).
  *
  * For every request b in [0, B) and head h it computes, in order:
- *   1. q_i, k_j: mean of Q / K over the valid tokens of block i / j
+ *   1. q_i, k_j: mean of Q over the valid tokens of q-block i (64 tokens) and
+ *      of K over those of kv block j (kv_block tokens, 64 or 128)
  *      (float64 accumulation, divided by the valid-token count);
  *   2. s_ij = sm_scale * <q_i, k_j> in float64;
  *   3. p_ij = softmax over j of s_ij;
  *   4. the order of j by (s_ij descending, j ascending);
  *   5. k_p = smallest k >= 1 whose cumulative p in that order is >= top_p
- *      (0 if top_p <= 0, n_blocks if top_p >= 1);
- *   6. k_min = ceil(min_top_k * n_blocks - 1e-9);
- *   7. keeps the first min(n_blocks, max(k_p, k_min, 1)) blocks of the order
+ *      (0 if top_p <= 0, n_kv if top_p >= 1);
+ *   6. k_min = ceil(min_top_k * n_kv - 1e-9);
+ *   7. keeps the first min(n_kv, max(k_p, k_min, 1)) blocks of the order
  *      and writes them ascending as CSR row (b * H + h) * n_blocks + i.
- * The result has mask_batch = B.  To build one mask from one request (and
- * reuse it for others), pass a B = 1 view of that request.
+ * The result has mask_batch = B and block = kv_block.  To build one mask from
+ * one request (and reuse it for others), pass a B = 1 view of that request.
  * key_scale     : optional first-frame key enhancement (NULL for none): the
  *                 pooled keys are those of the scaled K.
  *
  * q, k          : [B, S, H, D] f16 or bf16 (dtype), read only.
  * row_ptr       : out, device int32 [B * H * n_blocks + 1].
+ * kv_block      : 64 or 128 (else CHORUS_ERR_UNSUPPORTED).
  * col_idx       : out, device int32 [col_capacity]; col_capacity must be at
- *                 least B * H * n_blocks * n_blocks (the worst case, since the
+ *                 least B * H * n_blocks * n_kv (the worst case, since the
  *                 count is only known on device) else CHORUS_ERR_CAPACITY.
  * block_scores  : optional out (NULL to skip), device float32
- *                 [B * H * n_blocks, n_blocks]: s_ij rounded to fp32.
+ *                 [B * H * n_blocks, n_kv]: s_ij rounded to fp32.
  * workspace     : device scratch of at least
  *                 chorus_build_block_mask_workspace_size(shape) bytes,
  *                 256-byte aligned; contents on entry are ignored.
@@ -153,21 +159,22 @@ size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape);
 chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
                                       const chorus_tensor* q, const chorus_tensor* k,
                                       double sm_scale, double top_p, double min_top_k,
-                                      const chorus_key_scale* key_scale,
+                                      int32_t kv_block, const chorus_key_scale* key_scale,
                                       int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
                                       float* block_scores, void* workspace,
                                       size_t workspace_bytes, void* stream);
 
 /* The builder on fp8 input: q, k are e4m3fn codes [B, S, H, D] (uint8, strides
- * in bytes) with the fp32 block scales [B, H, n_blocks] of the quantiser;
- * step 1 pools the values code * scale (the block's scale is constant, so
- * the mean is scale * mean(code), in float64).  Everything else as
- * chorus_build_block_mask (same workspace size).  dtype CHORUS_FP8_E4M3 on
- * chorus_build_block_mask itself returns CHORUS_ERR_UNSUPPORTED. */
+ * in bytes) with the fp32 scales [B, H, n_blocks] of the quantiser (one per
+ * 64-token block); step 1 pools the values code * scale in float64.
+ * Everything else as chorus_build_block_mask (same workspace size).  dtype
+ * CHORUS_FP8_E4M3 on chorus_build_block_mask itself returns
+ * CHORUS_ERR_UNSUPPORTED. */
 chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const chorus_tensor* q,
                                           const float* q_scale, const chorus_tensor* k,
                                           const float* k_scale, double sm_scale, double top_p,
-                                          double min_top_k, const chorus_key_scale* key_scale,
+                                          double min_top_k, int32_t kv_block,
+                                          const chorus_key_scale* key_scale,
                                           int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
                                           float* block_scores, void* workspace,
                                           size_t workspace_bytes, void* stream);
@@ -179,7 +186,8 @@ chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const choru
  * be placed ahead of time.  The attention kernels deal their work to the 8
  * XCDs of the GPU in 8 equal runs of (request, head) units; the plan orders
  * the units so that those runs carry near-equal cost: units are taken
- * heaviest first (cost = listed blocks + q-blocks) and each goes to the
+ * heaviest first (cost = listed 64-token kv blocks + q-blocks, a kv block of
+ * 128 counting twice) and each goes to the
  * least-loaded XCD that still has room, the paper's greedy rule with the XCDs
  * in the role of the GPUs.  Within an XCD units keep ascending id, so the
  * workgroups running together share one head's K/V in that XCD's L2.
@@ -200,7 +208,7 @@ chorus_status chorus_plan_block_mask(const chorus_shape* shape, const chorus_blo
 /* ---------------------------------------------------------------------------
  * Mask check for masks that come from outside the builder.  Writes into
  * *d_flags (device int32, overwritten) the OR of: 1 = row_ptr[0] != 0,
- * 2 = row_ptr decreasing, 4 = col_idx out of [0, n_blocks),
+ * 2 = row_ptr decreasing, 4 = col_idx out of [0, n_kv),
  * 8 = col_idx not strictly ascending within a row, 16 = nnz > col_capacity.
  * 0 means valid.  Stream-ordered; the caller reads the flag when it needs it.
  * ------------------------------------------------------------------------- */
@@ -226,7 +234,7 @@ chorus_status chorus_quantize_fp8_blockwise(chorus_dtype in_dtype, const chorus_
  * for every request b, head h and query token r < S in q-block i, with mask
  * row m = ((mask_batch > 1 ? b : 0) * H + h) * n_blocks + i,
  *   O[b,r,h,:] = sum_{c in A} softmax_c(sm_scale <Q[b,r,h,:], K[b,c,h,:]>) V[b,c,h,:]
- * over A = { c < S : c / 64 listed in row m }, and
+ * over A = { c < S : c / mask->block listed in row m }, and
  *   lse[b,h,r] = ln sum_{c in A} exp(sm_scale <Q[b,r,h,:], K[b,c,h,:]>).
  * An empty row gives O = 0 and lse = -inf.
  *
@@ -297,7 +305,8 @@ chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const 
  * For every request b, head h, q-block i and kv-block j:
  *   mass[b,h,i,j] = (1 / |T_i|) * sum_{r in T_i} sum_{c in T_j}
  *                   exp(sm_scale <Q[b,r,h,:], K[b,c,h,:]> - lse[b,h,r])
- * where T_i are the valid tokens of block i and lse is the log-sum-exp of the
+ * where T_i are the valid tokens of q-block i (64 tokens), T_j those of kv
+ * block j (kv_block = 64 or 128 tokens), and lse is the log-sum-exp of the
  * DENSE attention of the same q and k with the same sm_scale (as written by
  * chorus_block_sparse_attn_fwd with mask = NULL).  Each row mass[b,h,i,:] is
  * then the mean attention distribution of q-block i over kv blocks (sums to
@@ -307,34 +316,36 @@ chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const 
  * lse   : device float32 [B, H, S], read only.
  * key_scale : optional first-frame key enhancement (NULL for none), as in
  *         the dense pass that wrote lse.
- * mass  : out, device float32 [B, H, n_blocks, n_blocks], row-major.
+ * mass  : out, device float32 [B, H, n_blocks, n_kv], row-major.
  * ------------------------------------------------------------------------- */
 chorus_status chorus_attn_block_mass(chorus_dtype dtype, const chorus_shape* shape,
                                      const chorus_tensor* q, const chorus_tensor* k, const float* lse,
-                                     float sm_scale, const chorus_key_scale* key_scale, float* mass,
-                                     void* stream);
+                                     float sm_scale, int32_t kv_block, const chorus_key_scale* key_scale,
+                                     float* mass, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Block mask from block masses (the selection of Sec. 3.2 "Mask Caching and
  * Retrieval" applied to an attention map): for every row mass[b,h,i,:]
  * (non-negative), blocks are ranked by (mass descending, j ascending) and the
- * first min(n, max(k_p, k_min, 1)) are kept, where k_p is the smallest k >= 1
- * whose share of the row's total mass is >= top_p (0 if top_p <= 0, n if
- * top_p >= 1) and k_min = ceil(min_top_k * n - 1e-9).  A row with zero total
+ * first min(n_kv, max(k_p, k_min, 1)) are kept, where k_p is the smallest
+ * k >= 1 whose share of the row's total mass is >= top_p (0 if top_p <= 0,
+ * n_kv if top_p >= 1) and k_min = ceil(min_top_k * n_kv - 1e-9).  A row with zero total
  * mass never reaches a top_p > 0, so it keeps every block (with top_p = 0 the
  * floor alone decides).  Output as chorus_build_block_mask (mask_batch = B).
  *
- * mass          : device float32 [B, H, n_blocks, n_blocks], read only.
+ * mass          : device float32 [B, H, n_blocks, n_kv], read only.
+ * kv_block      : the kv block size mass was taken with (64 or 128); the
+ *                 mask gets block = kv_block.
  * row_ptr       : out, device int32 [B * H * n_blocks + 1].
  * col_idx       : out, device int32 [col_capacity], col_capacity >=
- *                 B * H * n_blocks^2 (else CHORUS_ERR_CAPACITY).
+ *                 B * H * n_blocks * n_kv (else CHORUS_ERR_CAPACITY).
  * workspace     : device scratch of chorus_select_block_mask_workspace_size()
  *                 bytes, 256-byte aligned.
  * Supports n_blocks <= 4096.
  * ------------------------------------------------------------------------- */
 size_t chorus_select_block_mask_workspace_size(const chorus_shape* shape);
-chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* mass, double top_p,
-                                       double min_top_k, int32_t* row_ptr, int32_t* col_idx,
+chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* mass, int32_t kv_block,
+                                       double top_p, double min_top_k, int32_t* row_ptr, int32_t* col_idx,
                                        int64_t col_capacity, void* workspace, size_t workspace_bytes,
                                        void* stream);
 
@@ -345,10 +356,11 @@ chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* m
  *   coverage[b,h] = (1 / S) * sum_i |T_i| * sum_{j in row m} mass[b,h,i,j]
  * with m = ((mask_batch > 1 ? b : 0) * H + h) * n_blocks + i and mass as
  * written by chorus_attn_block_mass for those requests.  Ids outside
- * [0, n_blocks) are ignored.
+ * [0, n_kv) are ignored.
  *
  * mask     : the mask to judge (mask_batch 1 or B).
- * mass     : device float32 [B, H, n_blocks, n_blocks], read only.
+ * mass     : device float32 [B, H, n_blocks, n_kv] for the mask's kv block,
+ *            read only.
  * coverage : out, device float64 [B, H].
  * ------------------------------------------------------------------------- */
 chorus_status chorus_mask_coverage(const chorus_shape* shape, const chorus_block_mask* mask,
@@ -366,8 +378,10 @@ chorus_status chorus_mask_coverage(const chorus_shape* shape, const chorus_block
  *
  * V is a caller-owned device bitmap with one bit per (mask row, kv block):
  * row r = (b_m * H + h) * n_blocks + i owns the words [r * W, (r + 1) * W),
- * W = ceil(n_blocks / 32), bit j % 32 of word j / 32 is pair (row r, block j).
- * Its size in bytes is chorus_visit_map_bytes(mask_batch, H, n_blocks).
+ * W = ceil(n_kv / 32), bit j % 32 of word j / 32 is pair (row r, block j).
+ * Its size in bytes is chorus_visit_map_bytes(mask) (0 for an invalid
+ * mask description); every mask of a group shares mask_batch, H, n_blocks
+ * and block.
  * The three calls below are stream-ordered; V must not be shared by calls
  * running concurrently on different streams.
  *
@@ -376,14 +390,14 @@ chorus_status chorus_mask_coverage(const chorus_shape* shape, const chorus_block
  * chorus_visit_refresh : writes the group's last-layer mask
  *                        out = mask | ~V (per row, the blocks of the mask
  *                        plus every block V has not recorded), as a CSR
- *                        with the mask's mask_batch / H / n_blocks; ids
- *                        ascending.  V is not modified (call
+ *                        with the mask's mask_batch / H / n_blocks / block;
+ *                        ids ascending.  V is not modified (call
  *                        chorus_visit_update with the output to record it).
  *   row_ptr, col_idx, col_capacity : as chorus_build_block_mask
- *                        (col_capacity >= rows * n_blocks).
+ *                        (col_capacity >= rows * n_kv).
  *   workspace : chorus_visit_refresh_workspace_size(mask) bytes, 256-aligned.
  * ------------------------------------------------------------------------- */
-size_t chorus_visit_map_bytes(int32_t mask_batch, int32_t H, int32_t n_blocks);
+size_t chorus_visit_map_bytes(const chorus_block_mask* mask);
 chorus_status chorus_visit_reset(const chorus_block_mask* mask, uint32_t* visited, void* stream);
 chorus_status chorus_visit_update(const chorus_block_mask* mask, uint32_t* visited, void* stream);
 size_t chorus_visit_refresh_workspace_size(const chorus_block_mask* mask);

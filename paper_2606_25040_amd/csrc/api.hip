@@ -66,9 +66,19 @@ static bool offsets_fit(int32_t S, int64_t stride_s, size_t es) {
   return (int64_t)(S - 1) * stride_s * (int64_t)es + 256 <= (int64_t)UINT32_MAX;
 }
 
+// kv block sizes a mask may list: 64 (square blocks) or 128 (the paper's
+// kernel geometry, q-blocks of 64 with kv blocks of 128).
+static bool kv_block_ok(int32_t kvb) { return kvb == kBlock || kvb == 2 * kBlock; }
+
+// Columns of a mask: kv blocks per row.
+static int32_t mask_columns(const chorus_block_mask* m) {
+  return (int32_t)(((int64_t)m->n_blocks * kBlock + m->block - 1) / m->block);
+}
+
 static chorus_status check_mask(const chorus_shape* s, const chorus_block_mask* m) {
   if (!m) return fail(CHORUS_ERR_INVALID_ARG, "mask is NULL");
-  if (m->block != kBlock) return fail(CHORUS_ERR_UNSUPPORTED, "mask block %d unsupported (only 64)", m->block);
+  if (!kv_block_ok(m->block))
+    return fail(CHORUS_ERR_UNSUPPORTED, "mask kv block %d unsupported (64 or 128)", m->block);
   if (m->mask_batch != 1 && m->mask_batch != s->B)
     return fail(CHORUS_ERR_INVALID_ARG, "mask_batch %d must be 1 or B=%d", m->mask_batch, s->B);
   if (m->H != s->H) return fail(CHORUS_ERR_INVALID_ARG, "mask H=%d != shape H=%d", m->H, s->H);
@@ -146,7 +156,7 @@ size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape) {
 
 static chorus_status build_mask_impl(chorus_dtype dtype, const chorus_shape* shape, const chorus_tensor* q,
                                      const float* q_scale, const chorus_tensor* k, const float* k_scale,
-                                     double sm_scale, double top_p, double min_top_k,
+                                     double sm_scale, double top_p, double min_top_k, int32_t kv_block,
                                      const chorus_key_scale* key_scale, int32_t* row_ptr, int32_t* col_idx,
                                      int64_t col_capacity, float* block_scores, void* workspace,
                                      size_t workspace_bytes, void* stream) {
@@ -166,36 +176,40 @@ static chorus_status build_mask_impl(chorus_dtype dtype, const chorus_shape* sha
   if (!(min_top_k >= 0.0 && min_top_k <= 1.0))
     return fail(CHORUS_ERR_INVALID_ARG, "min_top_k must be in [0, 1]");
   if (!std::isfinite(sm_scale)) return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite");
+  if (!kv_block_ok(kv_block)) return fail(CHORUS_ERR_UNSUPPORTED, "kv_block %d unsupported (64 or 128)", kv_block);
   KeyScale ks;
   if ((st = check_key_scale(key_scale, shape->S, &ks))) return st;
   if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
+  const int nk = (shape->S + kv_block - 1) / kv_block;
   const int64_t rows = (int64_t)shape->B * shape->H * n;
-  if (rows * n > INT32_MAX)
-    return fail(CHORUS_ERR_UNSUPPORTED, "B*H*n_blocks^2 = %lld exceeds int32 CSR offsets", (long long)(rows * n));
-  if (col_capacity < rows * n)
+  if (rows * nk > INT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "rows*kv blocks = %lld exceeds int32 CSR offsets", (long long)(rows * nk));
+  if (col_capacity < rows * nk)
     return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
-                (long long)(rows * n));
+                (long long)(rows * nk));
   size_t need = 0;
-  BuilderWorkspace w = carve_builder(workspace, shape->B, shape->H, n, &need);
+  BuilderWorkspace w = carve_builder(workspace, shape->B, shape->H, n, &need);   // sized for nk <= n
   if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
-  const int k_min = (int)std::ceil(min_top_k * (double)n - 1e-9);
+  const int words = (nk + 31) / 32;
+  const int k_min = (int)std::ceil(min_top_k * (double)nk - 1e-9);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const hipError_t pe =
-      fp8 ? launch_pool_fp8(targ(q), q_scale, targ(k), k_scale, shape->B, shape->S, shape->H, ks, w.qbar, w.kbar, s)
-          : launch_pool(dtype, targ(q), targ(k), shape->B, shape->S, shape->H, ks, w.qbar, w.kbar, s);
+  const hipError_t pe = fp8 ? launch_pool_fp8(targ(q), q_scale, targ(k), k_scale, shape->B, shape->S, shape->H,
+                                              kv_block, ks, w.qbar, w.kbar, s)
+                            : launch_pool(dtype, targ(q), targ(k), shape->B, shape->S, shape->H, kv_block, ks,
+                                          w.qbar, w.kbar, s);
   if ((st = from_hip(pe, "pool"))) return st;
-  if ((st = from_hip(launch_score_select(w.qbar, w.kbar, shape->B, shape->H, n, sm_scale, top_p,
-                                         k_min, w.scores, w.counts, w.bitmap, w.words, block_scores, s),
+  if ((st = from_hip(launch_score_select(w.qbar, w.kbar, shape->B, shape->H, n, nk, sm_scale, top_p, k_min,
+                                         w.scores, w.counts, w.bitmap, words, block_scores, s),
                      "score_select")))
     return st;
   if ((st = from_hip(launch_scan_counts(w.counts, rows, row_ptr, s), "scan"))) return st;
-  return from_hip(launch_compact(w.bitmap, w.words, row_ptr, rows, col_idx, s), "compact");
+  return from_hip(launch_compact(w.bitmap, words, row_ptr, rows, col_idx, s), "compact");
 }
 
 chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
                                       const chorus_tensor* q, const chorus_tensor* k,
                                       double sm_scale, double top_p, double min_top_k,
-                                      const chorus_key_scale* key_scale,
+                                      int32_t kv_block, const chorus_key_scale* key_scale,
                                       int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
                                       float* block_scores, void* workspace,
                                       size_t workspace_bytes, void* stream) {
@@ -203,18 +217,20 @@ chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* sh
     g_last_error[0] = 0;
     return fail(CHORUS_ERR_UNSUPPORTED, "fp8 input goes through chorus_build_block_mask_fp8 (it needs scales)");
   }
-  return build_mask_impl(dtype, shape, q, nullptr, k, nullptr, sm_scale, top_p, min_top_k, key_scale, row_ptr,
-                         col_idx, col_capacity, block_scores, workspace, workspace_bytes, stream);
+  return build_mask_impl(dtype, shape, q, nullptr, k, nullptr, sm_scale, top_p, min_top_k, kv_block, key_scale,
+                         row_ptr, col_idx, col_capacity, block_scores, workspace, workspace_bytes, stream);
 }
 
 chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const chorus_tensor* q, const float* q_scale,
                                           const chorus_tensor* k, const float* k_scale, double sm_scale,
-                                          double top_p, double min_top_k, const chorus_key_scale* key_scale,
+                                          double top_p, double min_top_k, int32_t kv_block,
+                                          const chorus_key_scale* key_scale,
                                           int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
                                           float* block_scores, void* workspace, size_t workspace_bytes,
                                           void* stream) {
-  return build_mask_impl(CHORUS_FP8_E4M3, shape, q, q_scale, k, k_scale, sm_scale, top_p, min_top_k, key_scale,
-                         row_ptr, col_idx, col_capacity, block_scores, workspace, workspace_bytes, stream);
+  return build_mask_impl(CHORUS_FP8_E4M3, shape, q, q_scale, k, k_scale, sm_scale, top_p, min_top_k, kv_block,
+                         key_scale, row_ptr, col_idx, col_capacity, block_scores, workspace, workspace_bytes,
+                         stream);
 }
 
 size_t chorus_plan_workspace_size(const chorus_shape* shape, const chorus_block_mask* mask) {
@@ -232,8 +248,8 @@ chorus_status chorus_plan_block_mask(const chorus_shape* shape, const chorus_blo
   if ((st = check_mask(shape, mask))) return st;
   if (!order) return fail(CHORUS_ERR_INVALID_ARG, "order is NULL");
   if ((st = check_workspace(workspace, workspace_bytes, chorus_plan_workspace_size(shape, mask)))) return st;
-  return from_hip(launch_plan(mask->row_ptr, mask->mask_batch, shape->B, shape->H, mask->n_blocks, order,
-                              static_cast<hipStream_t>(stream)),
+  return from_hip(launch_plan(mask->row_ptr, mask->mask_batch, shape->B, shape->H, mask->n_blocks,
+                              mask->block / kBlock, order, static_cast<hipStream_t>(stream)),
                   "plan");
 }
 
@@ -244,8 +260,10 @@ chorus_status chorus_validate_block_mask(const chorus_block_mask* mask, int64_t 
     return fail(CHORUS_ERR_INVALID_ARG, "mask, its arrays and d_flags must be non-NULL");
   if (mask->mask_batch < 1 || mask->H < 1 || mask->n_blocks < 1)
     return fail(CHORUS_ERR_INVALID_ARG, "mask dimensions must be >= 1");
+  if (!kv_block_ok(mask->block))
+    return fail(CHORUS_ERR_UNSUPPORTED, "mask kv block %d unsupported (64 or 128)", mask->block);
   const int64_t rows = (int64_t)mask->mask_batch * mask->H * mask->n_blocks;
-  return from_hip(launch_validate(mask->row_ptr, mask->col_idx, rows, mask->n_blocks, col_capacity, d_flags,
+  return from_hip(launch_validate(mask->row_ptr, mask->col_idx, rows, mask_columns(mask), col_capacity, d_flags,
                                   static_cast<hipStream_t>(stream)),
                   "validate");
 }
@@ -306,6 +324,9 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   const int n = blocks_of(shape->S);
   const int64_t items = (int64_t)shape->B * shape->H * n;
   if (items > INT32_MAX) return fail(CHORUS_ERR_UNSUPPORTED, "too many work items");
+  // kv blocks of 128 are walked as 64-token halves: doubled CSR positions must fit int32
+  if (mask && mask->block != kBlock && (int64_t)mask->mask_batch * shape->H * n * mask_columns(mask) * 2 > INT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "mask too large for kv blocks of 128");
   if (!offsets_fit(shape->S, std::max(std::max(q->stride_s, k->stride_s), v->stride_s), es))
     return fail(CHORUS_ERR_UNSUPPORTED, "token stride too large for 32-bit in-head offsets");
   if (schedule) {
@@ -327,6 +348,7 @@ chorus_status chorus_block_sparse_attn_fwd(chorus_dtype dtype, const chorus_shap
   a.row_ptr = mask ? mask->row_ptr : nullptr;   // NULL row_ptr selects the dense kernel
   a.col_idx = mask ? mask->col_idx : nullptr;
   a.mask_batch = mask ? mask->mask_batch : 1;
+  a.kv_block = mask ? mask->block : kBlock;
   a.order = schedule ? schedule->order : nullptr;
   a.lse = lse;
   a.B = shape->B;
@@ -377,8 +399,8 @@ chorus_status chorus_block_sparse_attn_fwd_fp8(const chorus_shape* shape, const 
 
 chorus_status chorus_attn_block_mass(chorus_dtype dtype, const chorus_shape* shape,
                                      const chorus_tensor* q, const chorus_tensor* k, const float* lse,
-                                     float sm_scale, const chorus_key_scale* key_scale, float* mass,
-                                     void* stream) {
+                                     float sm_scale, int32_t kv_block, const chorus_key_scale* key_scale,
+                                     float* mass, void* stream) {
   g_last_error[0] = 0;
   chorus_status st;
   if ((st = check_shape(shape))) return st;
@@ -392,9 +414,11 @@ chorus_status chorus_attn_block_mass(chorus_dtype dtype, const chorus_shape* sha
   if (!offsets_fit(shape->S, k->stride_s, 2))
     return fail(CHORUS_ERR_UNSUPPORTED, "token stride too large for 32-bit in-head offsets");
   if (shape->H > 65535 || shape->B > 65535) return fail(CHORUS_ERR_UNSUPPORTED, "B or H above 65535");
+  if (!kv_block_ok(kv_block)) return fail(CHORUS_ERR_UNSUPPORTED, "kv_block %d unsupported (64 or 128)", kv_block);
   KeyScale ks;
   if ((st = check_key_scale(key_scale, shape->S, &ks))) return st;
-  return from_hip(launch_block_mass(dtype, targ(q), targ(k), lse, shape->B, shape->S, shape->H, sm_scale, ks, mass,
+  return from_hip(launch_block_mass(dtype, targ(q), targ(k), lse, shape->B, shape->S, shape->H, sm_scale, ks,
+                                    kv_block, mass,
                                     static_cast<hipStream_t>(stream)),
                   "block_mass");
 }
@@ -409,15 +433,17 @@ size_t chorus_select_block_mask_workspace_size(const chorus_shape* shape) {
   return align_up(c.used, 256);
 }
 
-chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* mass, double top_p,
-                                       double min_top_k, int32_t* row_ptr, int32_t* col_idx,
+chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* mass, int32_t kv_block,
+                                       double top_p, double min_top_k, int32_t* row_ptr, int32_t* col_idx,
                                        int64_t col_capacity, void* workspace, size_t workspace_bytes,
                                        void* stream) {
   g_last_error[0] = 0;
   chorus_status st;
   if ((st = check_shape(shape))) return st;
   if (!mass) return fail(CHORUS_ERR_INVALID_ARG, "mass is NULL");
+  if (!kv_block_ok(kv_block)) return fail(CHORUS_ERR_UNSUPPORTED, "kv_block %d unsupported (64 or 128)", kv_block);
   const int n = blocks_of(shape->S);
+  const int nk = (shape->S + kv_block - 1) / kv_block;
   if (n > kMaxBuilderBlocks)
     return fail(CHORUS_ERR_UNSUPPORTED, "n_blocks=%d exceeds selection limit %d", n, kMaxBuilderBlocks);
   if (!(top_p >= 0.0 && top_p <= 1.0)) return fail(CHORUS_ERR_INVALID_ARG, "top_p must be in [0, 1]");
@@ -425,19 +451,19 @@ chorus_status chorus_select_block_mask(const chorus_shape* shape, const float* m
     return fail(CHORUS_ERR_INVALID_ARG, "min_top_k must be in [0, 1]");
   if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
   const int64_t rows = (int64_t)shape->B * shape->H * n;
-  if (rows * n > INT32_MAX)
-    return fail(CHORUS_ERR_UNSUPPORTED, "B*H*n_blocks^2 = %lld exceeds int32 CSR offsets", (long long)(rows * n));
-  if (col_capacity < rows * n)
+  if (rows * nk > INT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "rows*kv blocks = %lld exceeds int32 CSR offsets", (long long)(rows * nk));
+  if (col_capacity < rows * nk)
     return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
-                (long long)(rows * n));
+                (long long)(rows * nk));
   if ((st = check_workspace(workspace, workspace_bytes, chorus_select_block_mask_workspace_size(shape)))) return st;
   Carver c(workspace);
   int32_t* counts = c.take<int32_t>(rows);
-  const int words = (n + 31) / 32;
-  uint32_t* bitmap = c.take<uint32_t>(rows * words);
-  const int k_min = (int)std::ceil(min_top_k * (double)n - 1e-9);
+  const int words = (nk + 31) / 32;
+  uint32_t* bitmap = c.take<uint32_t>(rows * words);   // the workspace is sized for nk <= n
+  const int k_min = (int)std::ceil(min_top_k * (double)nk - 1e-9);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = from_hip(launch_select_from_mass(mass, rows, n, top_p, k_min, counts, bitmap, words, s), "select")))
+  if ((st = from_hip(launch_select_from_mass(mass, rows, nk, top_p, k_min, counts, bitmap, words, s), "select")))
     return st;
   if ((st = from_hip(launch_scan_counts(counts, rows, row_ptr, s), "scan"))) return st;
   return from_hip(launch_compact(bitmap, words, row_ptr, rows, col_idx, s), "compact");
@@ -452,13 +478,14 @@ chorus_status chorus_mask_coverage(const chorus_shape* shape, const chorus_block
   if (!mass || !coverage) return fail(CHORUS_ERR_INVALID_ARG, "mass/coverage is NULL");
   if (shape->H > 65535 || shape->B > 65535) return fail(CHORUS_ERR_UNSUPPORTED, "B or H above 65535");
   return from_hip(launch_coverage(mask->row_ptr, mask->col_idx, mask->mask_batch, mass, shape->B, shape->S,
-                                  shape->H, coverage, static_cast<hipStream_t>(stream)),
+                                  shape->H, mask->block, coverage, static_cast<hipStream_t>(stream)),
                   "coverage");
 }
 
 static chorus_status check_mask_alone(const chorus_block_mask* m) {
   if (!m) return fail(CHORUS_ERR_INVALID_ARG, "mask is NULL");
-  if (m->block != kBlock) return fail(CHORUS_ERR_UNSUPPORTED, "mask block %d unsupported (only 64)", m->block);
+  if (!kv_block_ok(m->block))
+    return fail(CHORUS_ERR_UNSUPPORTED, "mask kv block %d unsupported (64 or 128)", m->block);
   if (m->mask_batch < 1 || m->H < 1 || m->n_blocks < 1)
     return fail(CHORUS_ERR_INVALID_ARG, "mask_batch/H/n_blocks must be >= 1");
   if (m->n_blocks > kMaxBuilderBlocks)
@@ -467,9 +494,12 @@ static chorus_status check_mask_alone(const chorus_block_mask* m) {
   return CHORUS_OK;
 }
 
-size_t chorus_visit_map_bytes(int32_t mask_batch, int32_t H, int32_t n_blocks) {
-  if (mask_batch < 1 || H < 1 || n_blocks < 1) return 0;
-  return (size_t)mask_batch * H * n_blocks * ((n_blocks + 31) / 32) * sizeof(uint32_t);
+// Words of one row of a visited map: one bit per column of the mask.
+static int64_t visit_words(const chorus_block_mask* m) { return (mask_columns(m) + 31) / 32; }
+
+size_t chorus_visit_map_bytes(const chorus_block_mask* mask) {
+  if (!mask || mask->mask_batch < 1 || mask->H < 1 || mask->n_blocks < 1 || !kv_block_ok(mask->block)) return 0;
+  return (size_t)mask->mask_batch * mask->H * mask->n_blocks * visit_words(mask) * sizeof(uint32_t);
 }
 
 chorus_status chorus_visit_reset(const chorus_block_mask* mask, uint32_t* visited, void* stream) {
@@ -477,7 +507,7 @@ chorus_status chorus_visit_reset(const chorus_block_mask* mask, uint32_t* visite
   chorus_status st;
   if ((st = check_mask_alone(mask))) return st;
   if (!visited) return fail(CHORUS_ERR_INVALID_ARG, "visited is NULL");
-  const int64_t words = (int64_t)mask->mask_batch * mask->H * mask->n_blocks * ((mask->n_blocks + 31) / 32);
+  const int64_t words = (int64_t)mask->mask_batch * mask->H * mask->n_blocks * visit_words(mask);
   return from_hip(launch_fill_u32(visited, 0u, words, static_cast<hipStream_t>(stream)), "visit_reset");
 }
 
@@ -487,17 +517,17 @@ chorus_status chorus_visit_update(const chorus_block_mask* mask, uint32_t* visit
   if ((st = check_mask_alone(mask))) return st;
   if (!visited) return fail(CHORUS_ERR_INVALID_ARG, "visited is NULL");
   const int64_t rows = (int64_t)mask->mask_batch * mask->H * mask->n_blocks;
-  return from_hip(launch_visit_update(mask->row_ptr, mask->col_idx, rows, mask->n_blocks, visited,
+  return from_hip(launch_visit_update(mask->row_ptr, mask->col_idx, rows, mask_columns(mask), visited,
                                       static_cast<hipStream_t>(stream)),
                   "visit_update");
 }
 
 size_t chorus_visit_refresh_workspace_size(const chorus_block_mask* mask) {
-  if (!mask || mask->mask_batch < 1 || mask->H < 1 || mask->n_blocks < 1) return 0;
+  if (!mask || mask->mask_batch < 1 || mask->H < 1 || mask->n_blocks < 1 || !kv_block_ok(mask->block)) return 0;
   const size_t rows = (size_t)mask->mask_batch * mask->H * mask->n_blocks;
   Carver c(nullptr);
   c.take<int32_t>(rows);
-  c.take<uint32_t>(rows * ((mask->n_blocks + 31) / 32));
+  c.take<uint32_t>(rows * visit_words(mask));
   return align_up(c.used, 256);
 }
 
@@ -509,20 +539,20 @@ chorus_status chorus_visit_refresh(const chorus_block_mask* mask, const uint32_t
   if ((st = check_mask_alone(mask))) return st;
   if (!visited) return fail(CHORUS_ERR_INVALID_ARG, "visited is NULL");
   if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
-  const int n = mask->n_blocks;
-  const int64_t rows = (int64_t)mask->mask_batch * mask->H * n;
-  if (rows * n > INT32_MAX)
-    return fail(CHORUS_ERR_UNSUPPORTED, "rows*n_blocks = %lld exceeds int32 CSR offsets", (long long)(rows * n));
-  if (col_capacity < rows * n)
+  const int nk = mask_columns(mask);
+  const int64_t rows = (int64_t)mask->mask_batch * mask->H * mask->n_blocks;
+  if (rows * nk > INT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "rows*columns = %lld exceeds int32 CSR offsets", (long long)(rows * nk));
+  if (col_capacity < rows * nk)
     return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
-                (long long)(rows * n));
+                (long long)(rows * nk));
   if ((st = check_workspace(workspace, workspace_bytes, chorus_visit_refresh_workspace_size(mask)))) return st;
   Carver c(workspace);
   int32_t* counts = c.take<int32_t>(rows);
-  const int words = (n + 31) / 32;
+  const int words = (int)visit_words(mask);
   uint32_t* bitmap = c.take<uint32_t>(rows * words);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if ((st = from_hip(launch_visit_refresh(mask->row_ptr, mask->col_idx, rows, n, visited, counts, bitmap, s),
+  if ((st = from_hip(launch_visit_refresh(mask->row_ptr, mask->col_idx, rows, nk, visited, counts, bitmap, s),
                      "visit_refresh")))
     return st;
   if ((st = from_hip(launch_scan_counts(counts, rows, row_ptr, s), "scan"))) return st;

@@ -74,7 +74,10 @@ __device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
 
 // Walk of the merged kv lists of the two q-blocks (2p, 2p + 1) of a pair in
 // ascending kv id, skipping ids outside [0, n).  All lanes hold the same
-// state (it lives in scalar registers).
+// state (it lives in scalar registers).  KV2: the lists hold kv blocks of 128
+// tokens and the walk visits both 64-token halves of each (positions of the
+// doubled list), so ids stay in 64-token units.
+template <bool KV2>
 struct PairWalk {
   ConstI32* col;
   int pa, a1, pb, b1, n;
@@ -95,10 +98,16 @@ struct PairWalk {
       a1 = a.row_ptr[r0 + ia + 1];
       pb = ib < n ? a.row_ptr[r0 + ib] : 0;
       b1 = ib < n ? a.row_ptr[r0 + ib + 1] : 0;
+      if (KV2) {
+        pa *= 2;
+        a1 *= 2;
+        pb *= 2;
+        b1 *= 2;
+      }
     }
   }
   __device__ bool listed(int sel) const { return sel == 0 ? a1 > pa : b1 > pb; }
-  __device__ int id_at(int p) const { return dense ? p : col[p]; }
+  __device__ int id_at(int p) const { return dense ? p : KV2 ? 2 * col[p >> 1] + (p & 1) : col[p]; }
   __device__ int head_a() {
     while (pa < a1) {
       const int j = id_at(pa);

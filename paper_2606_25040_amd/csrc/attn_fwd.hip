@@ -109,7 +109,7 @@ struct TileLoader {
   }
 };
 
-template <bool BF16, bool DENSE, bool KSCALE>
+template <bool BF16, bool DENSE, bool KSCALE, bool KV2>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
   using E = Elt<BF16>;
@@ -124,16 +124,23 @@ void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
   const int i = item % n;
   const int bh = item / n;
   const int h = bh % H, b = bh / H;
-  // DENSE: every kv block (no mask); otherwise the CSR row of (b, h, i)
+  // DENSE: every kv block (no mask); otherwise the CSR row of (b, h, i).
+  // KV2: the row lists kv blocks of 128 tokens; the walk visits both 64-token
+  // halves of each (positions 2 p and 2 p + 1 of the doubled list).
   int kb0 = 0, kb1 = n;
   if (!DENSE) {
     const int64_t mrow = ((int64_t)(a.mask_batch > 1 ? b : 0) * H + h) * n + i;
     kb0 = a.row_ptr[mrow];
     kb1 = a.row_ptr[mrow + 1];
+    if (KV2) {
+      kb0 *= 2;
+      kb1 *= 2;
+    }
   }
   ConstI32* cidx = as_constant(a.col_idx);   // scalar loads
-  auto kv_block = [&](int jj) { return DENSE ? jj : cidx[jj]; };
-  // ids outside [0, n) are skipped (the builder never emits them)
+  auto kv_block = [&](int jj) { return DENSE ? jj : KV2 ? 2 * cidx[jj >> 1] + (jj & 1) : cidx[jj]; };
+  // ids outside [0, n) are skipped (the builder never emits them; with KV2
+  // this also drops the missing half of a last block of 64 tokens)
   auto next_valid = [&](int jj) {
     while (jj < kb1) {
       const int j = kv_block(jj);
@@ -325,12 +332,22 @@ void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
 }  // namespace
 
 namespace {
-template <bool BF16, bool DENSE>
+template <bool BF16, bool DENSE, bool KV2>
 void launch_16(const AttnArgs& a, dim3 grid, int chunk, int W, hipStream_t st) {
   if (a.ks.n_first > 0)
-    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, true>), grid, dim3(128), 0, st, a, chunk, W);
+    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, true, KV2>), grid, dim3(128), 0, st, a, chunk, W);
   else
-    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, false>), grid, dim3(128), 0, st, a, chunk, W);
+    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, false, KV2>), grid, dim3(128), 0, st, a, chunk, W);
+}
+
+template <bool BF16>
+void launch_16_mask(const AttnArgs& a, dim3 grid, int chunk, int W, hipStream_t st) {
+  if (a.row_ptr == nullptr)
+    launch_16<BF16, true, false>(a, grid, chunk, W, st);
+  else if (a.kv_block == 2 * kBlock)
+    launch_16<BF16, false, true>(a, grid, chunk, W, st);
+  else
+    launch_16<BF16, false, false>(a, grid, chunk, W, st);
 }
 }  // namespace
 
@@ -338,18 +355,10 @@ hipError_t launch_attn_fwd_16(chorus_dtype dt, const AttnArgs& a, hipStream_t st
   const int W = a.B * a.H * a.n;
   const int chunk = (W + kNumXcd - 1) / kNumXcd;
   const dim3 grid(chunk * kNumXcd);
-  const bool dense = a.row_ptr == nullptr;
-  if (dt == CHORUS_BF16) {
-    if (dense)
-      launch_16<true, true>(a, grid, chunk, W, st);
-    else
-      launch_16<true, false>(a, grid, chunk, W, st);
-  } else {
-    if (dense)
-      launch_16<false, true>(a, grid, chunk, W, st);
-    else
-      launch_16<false, false>(a, grid, chunk, W, st);
-  }
+  if (dt == CHORUS_BF16)
+    launch_16_mask<true>(a, grid, chunk, W, st);
+  else
+    launch_16_mask<false>(a, grid, chunk, W, st);
   return hipGetLastError();
 }
 

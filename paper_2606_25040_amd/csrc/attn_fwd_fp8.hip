@@ -59,7 +59,7 @@ __device__ inline void load_tile8(uint32_t lds, const char* base, uint32_t ss, i
   }
 }
 
-template <bool DENSE, bool KSCALE>
+template <bool DENSE, bool KSCALE, bool KV2>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
   __shared__ __attribute__((aligned(1024))) uint8_t tiles[2][2][kTile8];   // [buffer][K, V]
@@ -83,7 +83,7 @@ void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
   ConstF32* ksc = as_constant(a.k_scale) + (int64_t)bh * n;
   ConstF32* vsc = as_constant(a.v_scale) + (int64_t)bh * n;
 
-  PairWalk walk;
+  PairWalk<KV2> walk;
   walk.init(a, DENSE, b, h, ip);
   const bool listed_any = q_active && walk.listed(sel);
 
@@ -285,14 +285,19 @@ hipError_t launch_attn_fwd_fp8(const AttnArgs& a, hipStream_t st) {
   const bool ks = a.ks.n_first > 0;
   if (a.row_ptr == nullptr) {
     if (ks)
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, true>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, true, false>), grid, block, 0, st, a, chunk, W, np);
     else
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, false>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, false, false>), grid, block, 0, st, a, chunk, W, np);
+  } else if (a.kv_block == 2 * kBlock) {
+    if (ks)
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, true, true>), grid, block, 0, st, a, chunk, W, np);
+    else
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, false, true>), grid, block, 0, st, a, chunk, W, np);
   } else {
     if (ks)
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, true>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, true, false>), grid, block, 0, st, a, chunk, W, np);
     else
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, false>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, false, false>), grid, block, 0, st, a, chunk, W, np);
   }
   return hipGetLastError();
 }

@@ -9,7 +9,8 @@
 // scores of one query), turns the scores into the dense attention
 // probabilities with the log-sum-exp of the dense forward pass,
 // p = 2^(s log2(e) sm_scale - lse log2(e)), and sums them over the block's
-// queries and keys: mass[i, j] = sum / |T_i|.  K tiles are double-buffered in
+// queries and keys: mass[i, j] = sum / |T_i|.  For kv blocks of 128 tokens the
+// sums of the two 64-key halves are added before the division.  K tiles are double-buffered in
 // LDS with direct global -> LDS loads; one barrier per kv block, which also
 // publishes the two waves' partial sums.
 #include "attn_common.h"
@@ -56,7 +57,7 @@ __device__ inline void load_k_half(uint32_t lds, const char* base, uint32_t ss, 
 template <bool BF16>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
 void block_mass_kernel(TensorArg q, TensorArg k, const float* __restrict__ lse, int S, int H, int n,
-                       float sm_scale, KeyScale ks, float* __restrict__ mass) {
+                       float sm_scale, KeyScale ks, bool kv2, float* __restrict__ mass) {
   using E = MassElt<BF16>;
   using vec8 = typename E::vec8;
   using scalar = typename E::scalar;
@@ -98,7 +99,10 @@ void block_mass_kernel(TensorArg q, TensorArg k, const float* __restrict__ lse, 
 
   const int k_row_off = l32 * 256;
   const int k_swzl = l32 & 15;
-  float* out = mass + (((int64_t)b * H + h) * n + i) * n;
+  // kv2: kv blocks of 128 tokens, each the sum of two 64-token halves
+  const int nk = kv2 ? (n + 1) / 2 : n;
+  float* out = mass + (((int64_t)b * H + h) * n + i) * nk;
+  float half = 0.f;   // first half of the current 128-token block (thread 0)
   for (int j = 0; j < n; ++j) {
     if (j + 1 < n) load_k_half(lds0 + ((j + 1) & 1) * kMassTile, kbase, kss, j + 1, S, wave, lane);
     const char* kt = &k_s[j & 1][0];
@@ -140,7 +144,18 @@ void block_mass_kernel(TensorArg q, TensorArg k, const float* __restrict__ lse, 
     if (lane == 0) red[j & 1][wave] = sum;
     CHORUS_WAIT_VMCNT(0);   // K_{j+1} landed
     __syncthreads();
-    if (tid == 0) out[j] = (red[j & 1][0] + red[j & 1][1]) / cnt_i;
+    if (tid == 0) {
+      const float v = red[j & 1][0] + red[j & 1][1];
+      if (!kv2) {
+        out[j] = v / cnt_i;
+      } else if (j & 1) {
+        out[j >> 1] = (half + v) / cnt_i;
+      } else if (j == n - 1) {
+        out[j >> 1] = v / cnt_i;
+      } else {
+        half = v;
+      }
+    }
   }
 }
 
@@ -149,19 +164,19 @@ void block_mass_kernel(TensorArg q, TensorArg k, const float* __restrict__ lse, 
 // valid-token counts, in float64.
 __global__ __launch_bounds__(256) void coverage_kernel(const int32_t* __restrict__ row_ptr,
                                                        const int32_t* __restrict__ col_idx, int mask_batch,
-                                                       const float* __restrict__ mass, int S, int H, int n,
+                                                       const float* __restrict__ mass, int S, int H, int n, int nk,
                                                        double* __restrict__ coverage) {
   __shared__ double red[4];
   const int h = blockIdx.x, b = blockIdx.y;
   const int tid = threadIdx.x;
-  const float* mb = mass + ((int64_t)b * H + h) * n * n;
+  const float* mb = mass + ((int64_t)b * H + h) * n * nk;
   double acc = 0.0;
   for (int i = tid; i < n; i += 256) {
     const int64_t r = ((int64_t)(mask_batch > 1 ? b : 0) * H + h) * n + i;
     double row = 0.0;
     for (int e = row_ptr[r]; e < row_ptr[r + 1]; ++e) {
       const int j = col_idx[e];
-      if (j >= 0 && j < n) row += (double)mb[(int64_t)i * n + j];
+      if (j >= 0 && j < nk) row += (double)mb[(int64_t)i * nk + j];
     }
     acc += row * (double)min(kBlock, S - i * kBlock);
   }
@@ -174,20 +189,21 @@ __global__ __launch_bounds__(256) void coverage_kernel(const int32_t* __restrict
 }  // namespace
 
 hipError_t launch_block_mass(chorus_dtype dt, TensorArg q, TensorArg k, const float* lse, int B, int S, int H,
-                             float sm_scale, KeyScale ks, float* mass, hipStream_t st) {
+                             float sm_scale, KeyScale ks, int kvb, float* mass, hipStream_t st) {
+  const bool kv2 = kvb == 2 * kBlock;
   const int n = blocks_of(S);
   const dim3 grid(n, H, B), block(128);
   if (dt == CHORUS_BF16)
-    hipLaunchKernelGGL(block_mass_kernel<true>, grid, block, 0, st, q, k, lse, S, H, n, sm_scale, ks, mass);
+    hipLaunchKernelGGL(block_mass_kernel<true>, grid, block, 0, st, q, k, lse, S, H, n, sm_scale, ks, kv2, mass);
   else
-    hipLaunchKernelGGL(block_mass_kernel<false>, grid, block, 0, st, q, k, lse, S, H, n, sm_scale, ks, mass);
+    hipLaunchKernelGGL(block_mass_kernel<false>, grid, block, 0, st, q, k, lse, S, H, n, sm_scale, ks, kv2, mass);
   return hipGetLastError();
 }
 
 hipError_t launch_coverage(const int32_t* row_ptr, const int32_t* col_idx, int mask_batch, const float* mass, int B,
-                           int S, int H, double* coverage, hipStream_t st) {
-  const int n = blocks_of(S);
-  hipLaunchKernelGGL(coverage_kernel, dim3(H, B), dim3(256), 0, st, row_ptr, col_idx, mask_batch, mass, S, H, n,
+                           int S, int H, int kvb, double* coverage, hipStream_t st) {
+  const int n = blocks_of(S), nk = (S + kvb - 1) / kvb;
+  hipLaunchKernelGGL(coverage_kernel, dim3(H, B), dim3(256), 0, st, row_ptr, col_idx, mask_batch, mass, S, H, n, nk,
                      coverage);
   return hipGetLastError();
 }

@@ -59,11 +59,11 @@ struct BuilderWorkspace {
   int32_t words;
 };
 BuilderWorkspace carve_builder(void* ws, int B, int H, int n, size_t* bytes);
-hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, KeyScale ks,
+hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, int kvb, KeyScale ks,
                        double* qbar, double* kbar, hipStream_t st);
 hipError_t launch_pool_fp8(TensorArg q, const float* q_scale, TensorArg k, const float* k_scale, int B, int S,
-                           int H, KeyScale ks, double* qbar, double* kbar, hipStream_t st);
-hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n,
+                           int H, int kvb, KeyScale ks, double* qbar, double* kbar, hipStream_t st);
+hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n, int nk,
                                double sm_scale, double top_p, int k_min, double* scores,
                                int32_t* counts, uint32_t* bitmap, int words, float* block_scores,
                                hipStream_t st);
@@ -72,16 +72,16 @@ hipError_t launch_select_from_mass(const float* mass, int64_t rows, int n, doubl
 hipError_t launch_scan_counts(const int32_t* counts, int64_t rows, int32_t* row_ptr, hipStream_t st);
 hipError_t launch_compact(const uint32_t* bitmap, int words, const int32_t* row_ptr, int64_t rows,
                           int32_t* col_idx, hipStream_t st);
-hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n, int32_t* order,
+hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n, int per_id, int32_t* order,
                        hipStream_t st);
 hipError_t launch_validate(const int32_t* row_ptr, const int32_t* col_idx, int64_t rows, int n,
                            int64_t capacity, int32_t* flags, hipStream_t st);
 
 // ---- block mass and coverage (block_mass.hip) ----
 hipError_t launch_block_mass(chorus_dtype dt, TensorArg q, TensorArg k, const float* lse, int B, int S, int H,
-                             float sm_scale, KeyScale ks, float* mass, hipStream_t st);
+                             float sm_scale, KeyScale ks, int kvb, float* mass, hipStream_t st);
 hipError_t launch_coverage(const int32_t* row_ptr, const int32_t* col_idx, int mask_batch, const float* mass, int B,
-                           int S, int H, double* coverage, hipStream_t st);
+                           int S, int H, int kvb, double* coverage, hipStream_t st);
 
 // ---- visit refreshing (fallback.hip) ----
 hipError_t launch_visit_update(const int32_t* row_ptr, const int32_t* col_idx, int64_t rows, int n,
@@ -106,6 +106,7 @@ struct AttnArgs {
   float* lse;             // nullable
   int B, S, H, n;
   int mask_batch;
+  int kv_block;           // tokens per listed kv block: 64, or 128 (two 64-token halves)
   float sm_scale;
   KeyScale ks;
 };

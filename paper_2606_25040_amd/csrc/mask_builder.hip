@@ -25,17 +25,21 @@ __device__ inline float to_f32(uint16_t bits, bool is_bf16) {
 // (g, c) with g = lane / 16 over token residues mod 4 and c = lane % 16 over
 // 16-byte column chunks; float64 partial sums, reduced over g by shuffles.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int S, int H, int n, bool bf16,
-                                                   KeyScale ks, double* __restrict__ qbar,
+__global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int S, int H, int n, int kvb, int nk,
+                                                   bool bf16, KeyScale ks, double* __restrict__ qbar,
                                                    double* __restrict__ kbar) {
   const int blk = blockIdx.x, h = blockIdx.y;
   const int b = blockIdx.z >> 1, which = blockIdx.z & 1;
+  // queries pool over 64-token blocks, keys over kvb-token blocks (nk of them)
+  const int bs = which ? kvb : kBlock;
+  const int nb = which ? nk : n;
+  if (blk >= nb) return;
   const TensorArg t = which ? k : q;
   double* out = which ? kbar : qbar;
   const int lane = threadIdx.x;
   const int g = lane >> 4, c = lane & 15;
-  const int t0 = blk * kBlock;
-  const int cnt = min(kBlock, S - t0);
+  const int t0 = blk * bs;
+  const int cnt = min(bs, S - t0);
   const uint16_t* base = static_cast<const uint16_t*>(t.data) + (int64_t)b * t.sb + (int64_t)h * t.sh + c * 8;
   double acc[8];
 #pragma unroll
@@ -60,7 +64,7 @@ __global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int 
     acc[e] += __shfl_xor(acc[e], 32);
   }
   if (g == 0) {
-    double* dst = out + ((int64_t)(b * H + h) * n + blk) * kHeadDim + c * 8;
+    double* dst = out + ((int64_t)(b * H + h) * nb + blk) * kHeadDim + c * 8;
 #pragma unroll
     for (int e = 0; e < 8; ++e) dst[e] = acc[e] / (double)cnt;
   }
@@ -75,23 +79,26 @@ __device__ inline float e4m3_to_f32(uint32_t c) {
   return (c & 0x80u) ? -mag : mag;
 }
 
-// 1b. Block mean-pool of fp8 e4m3 codes with per-(request, head, block)
-// scales, as written by the fp8 quantiser: the mean of code * scale over the
-// block's valid tokens, summed over codes in float64 and scaled once.  Same
-// lane layout as pool_kernel, eight codes (8 bytes) per lane and token.
+// 1b. Block mean-pool of fp8 e4m3 codes with per-(request, head, 64-token
+// block) scales, as written by the fp8 quantiser: the mean of code * scale
+// over the block's valid tokens, in float64.  Same lane layout as
+// pool_kernel, eight codes (8 bytes) per lane and token.
 __global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* __restrict__ q_scale, TensorArg k,
                                                       const float* __restrict__ k_scale, int S, int H, int n,
-                                                      KeyScale ks, double* __restrict__ qbar,
+                                                      int kvb, int nk, KeyScale ks, double* __restrict__ qbar,
                                                       double* __restrict__ kbar) {
   const int blk = blockIdx.x, h = blockIdx.y;
   const int b = blockIdx.z >> 1, which = blockIdx.z & 1;
+  const int bs = which ? kvb : kBlock;
+  const int nb = which ? nk : n;
+  if (blk >= nb) return;
   const TensorArg t = which ? k : q;
-  const float* sc = which ? k_scale : q_scale;
+  const float* sc = (which ? k_scale : q_scale) + ((int64_t)b * H + h) * n;   // per 64-token block
   double* out = which ? kbar : qbar;
   const int lane = threadIdx.x;
   const int g = lane >> 4, c = lane & 15;
-  const int t0 = blk * kBlock;
-  const int cnt = min(kBlock, S - t0);
+  const int t0 = blk * bs;
+  const int cnt = min(bs, S - t0);
   const uint8_t* base = static_cast<const uint8_t*>(t.data) + (int64_t)b * t.sb + (int64_t)h * t.sh + c * 8;
   double acc[8];
 #pragma unroll
@@ -100,7 +107,8 @@ __global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* 
   const double beta = (double)ks.beta;
   for (int tok = g; tok < cnt; tok += 4) {
     const uint2 raw = *reinterpret_cast<const uint2*>(base + (int64_t)(t0 + tok) * t.ss);
-    const double wt = t0 + tok < n_scaled ? beta : 1.0;
+    // the token's value is code * (scale of its 64-token block)
+    const double wt = (t0 + tok < n_scaled ? beta : 1.0) * (double)sc[(t0 + tok) / kBlock];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const uint32_t word = e < 4 ? raw.x : raw.y;
@@ -113,16 +121,15 @@ __global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* 
     acc[e] += __shfl_xor(acc[e], 32);
   }
   if (g == 0) {
-    const double scale = (double)sc[((int64_t)b * H + h) * n + blk];
-    double* dst = out + ((int64_t)(b * H + h) * n + blk) * kHeadDim + c * 8;
+    double* dst = out + ((int64_t)(b * H + h) * nb + blk) * kHeadDim + c * 8;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) dst[e] = acc[e] * scale / (double)cnt;
+    for (int e = 0; e < 8; ++e) dst[e] = acc[e] / (double)cnt;
   }
 }
 
 // ---------------------------------------------------------------------------
-// 2a. Block scores s = sm_scale * qbar kbar^T per (request, head): a float64
-// GEMM tile of 128 x 128 outputs per workgroup of 256 threads (8 x 8 outputs
+// 2a. Block scores s = sm_scale * qbar kbar^T per (request, head), n x nk
+// (q-blocks x kv blocks): a float64 GEMM tile of 128 x 128 outputs per workgroup of 256 threads (8 x 8 outputs
 // per thread, rows ti + 16 a, columns tj + 16 c), the k-dim staged through
 // LDS in chunks of 16.  Writes float64 scores into the workspace and,
 // optionally, fp32 copies.
@@ -131,14 +138,14 @@ constexpr int kST = 128;  // score tile
 constexpr int kSK = 16;   // k-chunk
 
 __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ qbar,
-                                                    const double* __restrict__ kbar, int n, double sm_scale,
+                                                    const double* __restrict__ kbar, int n, int nk, double sm_scale,
                                                     double* __restrict__ scores, float* __restrict__ scores32) {
   __shared__ double qs[kSK][kST + 2];
   __shared__ double ks[kSK][kST + 2];
   const int bh = blockIdx.z;
   const int i0 = blockIdx.y * kST, j0 = blockIdx.x * kST;
   const double* qb = qbar + (int64_t)bh * n * kHeadDim;
-  const double* kb = kbar + (int64_t)bh * n * kHeadDim;
+  const double* kb = kbar + (int64_t)bh * nk * kHeadDim;
   const int tid = threadIdx.x;
   const int ti = tid / 16, tj = tid % 16;
   double acc[8][8];
@@ -150,7 +157,7 @@ __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ q
     // 128 rows x 16 dims of each operand: thread -> (row, 8-dim half) pairs
     for (int e = tid; e < kST * 2; e += 256) {
       const int r = e >> 1, d0 = (e & 1) * 8;
-      const bool qin = i0 + r < n, kin = j0 + r < n;
+      const bool qin = i0 + r < n, kin = j0 + r < nk;
 #pragma unroll
       for (int d = 0; d < 8; ++d) {
         qs[d0 + d][r] = qin ? qb[(int64_t)(i0 + r) * kHeadDim + kk + d0 + d] : 0.0;
@@ -179,9 +186,9 @@ __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ q
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
       const int j = j0 + tj + 16 * c;
-      if (j >= n) continue;
+      if (j >= nk) continue;
       const double v = sm_scale * acc[a][c];
-      const int64_t o = ((int64_t)bh * n + i) * n + j;
+      const int64_t o = ((int64_t)bh * n + i) * nk + j;
       scores[o] = v;
       if (scores32) scores32[o] = (float)v;
     }
@@ -807,7 +814,8 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// 5. Work plan: head units u = b * H + h with cost sum_i (blocks(b,h,i) + 1)
+// 5. Work plan: head units u = b * H + h with cost sum_i (blocks(b,h,i) + 1),
+// a listed kv block counting as per_id 64-token blocks (2 for kv blocks of 128),
 // are assigned to the 8 XCDs greedily, heaviest first, each to the
 // least-loaded XCD that still has room (equal unit counts per XCD); the order
 // lists the units XCD by XCD, ascending unit id inside an XCD.  One
@@ -818,7 +826,7 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict
 constexpr int kPlanMaxUnits = 4096;
 
 __global__ __launch_bounds__(256) void plan_kernel(const int32_t* __restrict__ row_ptr, int mask_batch, int B,
-                                                   int H, int n, int32_t* __restrict__ order) {
+                                                   int H, int n, int per_id, int32_t* __restrict__ order) {
   __shared__ int32_t cost[kPlanMaxUnits];
   __shared__ int32_t by_cost[kPlanMaxUnits];
   __shared__ uint8_t xcd_of[kPlanMaxUnits];
@@ -831,7 +839,7 @@ __global__ __launch_bounds__(256) void plan_kernel(const int32_t* __restrict__ r
   for (int u = tid; u < U; u += 256) {
     const int b = u / H, h = u % H;
     const int64_t r0 = ((int64_t)(mask_batch > 1 ? b : 0) * H + h) * n;
-    cost[u] = row_ptr[r0 + n] - row_ptr[r0] + n;
+    cost[u] = (row_ptr[r0 + n] - row_ptr[r0]) * per_id + n;
   }
   __syncthreads();
   for (int u = tid; u < U; u += 256) {
@@ -916,18 +924,18 @@ __global__ __launch_bounds__(256) void validate_kernel(const int32_t* __restrict
 }  // namespace
 
 hipError_t launch_pool_fp8(TensorArg q, const float* q_scale, TensorArg k, const float* k_scale, int B, int S,
-                           int H, KeyScale ks, double* qbar, double* kbar, hipStream_t st) {
-  const int n = blocks_of(S);
-  hipLaunchKernelGGL(pool_fp8_kernel, dim3(n, H, 2 * B), dim3(64), 0, st, q, q_scale, k, k_scale, S, H, n, ks, qbar,
-                     kbar);
+                           int H, int kvb, KeyScale ks, double* qbar, double* kbar, hipStream_t st) {
+  const int n = blocks_of(S), nk = (S + kvb - 1) / kvb;
+  hipLaunchKernelGGL(pool_fp8_kernel, dim3(n, H, 2 * B), dim3(64), 0, st, q, q_scale, k, k_scale, S, H, n, kvb, nk,
+                     ks, qbar, kbar);
   return hipGetLastError();
 }
 
-hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, KeyScale ks,
+hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, int H, int kvb, KeyScale ks,
                        double* qbar, double* kbar, hipStream_t st) {
-  const int n = blocks_of(S);
-  hipLaunchKernelGGL(pool_kernel, dim3(n, H, 2 * B), dim3(64), 0, st, q, k, S, H, n, dt == CHORUS_BF16, ks,
-                     qbar, kbar);
+  const int n = blocks_of(S), nk = (S + kvb - 1) / kvb;
+  hipLaunchKernelGGL(pool_kernel, dim3(n, H, 2 * B), dim3(64), 0, st, q, k, S, H, n, kvb, nk, dt == CHORUS_BF16,
+                     ks, qbar, kbar);
   return hipGetLastError();
 }
 
@@ -957,15 +965,15 @@ hipError_t launch_select(const void* in, int64_t rows, int n, double top_p, int 
 }
 }  // namespace
 
-hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n, double sm_scale,
-                               double top_p, int k_min, double* scores, int32_t* counts, uint32_t* bitmap,
-                               int words, float* block_scores, hipStream_t st) {
-  const int tiles = (n + kST - 1) / kST;
-  hipLaunchKernelGGL(score_kernel, dim3(tiles, tiles, B * H), dim3(256), 0, st, qbar, kbar, n, sm_scale, scores,
-                     block_scores);
+hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n, int nk,
+                               double sm_scale, double top_p, int k_min, double* scores, int32_t* counts,
+                               uint32_t* bitmap, int words, float* block_scores, hipStream_t st) {
+  const int tiles_q = (n + kST - 1) / kST, tiles_k = (nk + kST - 1) / kST;
+  hipLaunchKernelGGL(score_kernel, dim3(tiles_k, tiles_q, B * H), dim3(256), 0, st, qbar, kbar, n, nk, sm_scale,
+                     scores, block_scores);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_select<false>(scores, (int64_t)B * H * n, n, top_p, k_min, counts, bitmap, words, st);
+  return launch_select<false>(scores, (int64_t)B * H * n, nk, top_p, k_min, counts, bitmap, words, st);
 }
 
 hipError_t launch_select_from_mass(const float* mass, int64_t rows, int n, double top_p, int k_min,
@@ -986,9 +994,9 @@ hipError_t launch_compact(const uint32_t* bitmap, int words, const int32_t* row_
   return hipGetLastError();
 }
 
-hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n, int32_t* order,
+hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int n, int per_id, int32_t* order,
                        hipStream_t st) {
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(256), 0, st, row_ptr, mask_batch, B, H, n, order);
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(256), 0, st, row_ptr, mask_batch, B, H, n, per_id, order);
   return hipGetLastError();
 }
 

@@ -87,9 +87,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.c_int64, ctypes.c_float, ctypes.c_double, ctypes.c_size_t)
     sig = {
         "chorus_build_block_mask_workspace_size": (SZ, [P(Shape)]),
-        "chorus_build_block_mask": (I32, [I32, P(Shape), P(Tensor), P(Tensor), F64, F64, F64,
+        "chorus_build_block_mask": (I32, [I32, P(Shape), P(Tensor), P(Tensor), F64, F64, F64, I32,
                                           P(KeyScale), VP, VP, I64, VP, VP, SZ, VP]),
-        "chorus_build_block_mask_fp8": (I32, [P(Shape), P(Tensor), VP, P(Tensor), VP, F64, F64, F64,
+        "chorus_build_block_mask_fp8": (I32, [P(Shape), P(Tensor), VP, P(Tensor), VP, F64, F64, F64, I32,
                                               P(KeyScale), VP, VP, I64, VP, VP, SZ, VP]),
         "chorus_plan_workspace_size": (SZ, [P(Shape), P(Mask)]),
         "chorus_plan_block_mask": (I32, [P(Shape), P(Mask), VP, VP, SZ, VP]),
@@ -108,12 +108,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "chorus_block_sparse_attn_fwd_fp8": (I32, [P(Shape), P(Tensor), P(Tensor), P(Tensor), VP,
                                                    VP, VP, P(Mask), P(Schedule), F32, P(KeyScale),
                                                    P(Tensor), VP, VP, SZ, VP]),
-        "chorus_attn_block_mass": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, F32, P(KeyScale),
-                                         VP, VP]),
+        "chorus_attn_block_mass": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, F32, I32,
+                                         P(KeyScale), VP, VP]),
         "chorus_select_block_mask_workspace_size": (SZ, [P(Shape)]),
-        "chorus_select_block_mask": (I32, [P(Shape), VP, F64, F64, VP, VP, I64, VP, SZ, VP]),
+        "chorus_select_block_mask": (I32, [P(Shape), VP, I32, F64, F64, VP, VP, I64, VP, SZ, VP]),
         "chorus_mask_coverage": (I32, [P(Shape), P(Mask), VP, VP, VP]),
-        "chorus_visit_map_bytes": (SZ, [I32, I32, I32]),
+        "chorus_visit_map_bytes": (SZ, [P(Mask)]),
         "chorus_visit_reset": (I32, [P(Mask), VP, VP]),
         "chorus_visit_update": (I32, [P(Mask), VP, VP]),
         "chorus_visit_refresh_workspace_size": (SZ, [P(Mask)]),
@@ -199,12 +199,17 @@ class BlockMask:
         return self.mask_batch * self.H * self.n_blocks
 
     @property
+    def n_kv(self) -> int:
+        """Columns: kv blocks of ``block`` tokens per row."""
+        return (self.n_blocks * BLOCK + self.block - 1) // self.block
+
+    @property
     def nnz(self) -> int:
         return int(self.row_ptr[-1].item())
 
     @property
     def density(self) -> float:
-        return self.nnz / float(self.rows * self.n_blocks)
+        return self.nnz / float(self.rows * self.n_kv)
 
     def as_c(self) -> Mask:
         return Mask(self.mask_batch, self.H, self.n_blocks, self.block, self.row_ptr.data_ptr(),
@@ -216,22 +221,24 @@ class BlockMask:
         return rp, self.col_idx[: int(rp[-1])].cpu().numpy().astype("int64")
 
     @staticmethod
-    def from_host(row_ptr, col_idx, mask_batch: int, H: int, n_blocks: int, device="cuda"):
+    def from_host(row_ptr, col_idx, mask_batch: int, H: int, n_blocks: int, device="cuda",
+                  block: int = BLOCK):
         rp = torch.as_tensor(row_ptr, dtype=torch.int32).to(device)
         ci = torch.as_tensor(col_idx, dtype=torch.int32)
         if ci.numel() == 0:
             ci = torch.zeros(1, dtype=torch.int32)
-        return BlockMask(rp, ci.to(device), mask_batch, H, n_blocks)
+        return BlockMask(rp, ci.to(device), mask_batch, H, n_blocks, block)
 
 
 def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: float,
                      sm_scale: float | None = None, return_scores: bool = False,
                      out: BlockMask | None = None, workspace: torch.Tensor | None = None,
-                     key_scale=None, scales=None) -> BlockMask:
+                     key_scale=None, scales=None, kv_block: int = BLOCK) -> BlockMask:
     """chorus_build_block_mask: one mask per request of ``q, k [B, S, H, D]``;
     ``key_scale = (n_first, beta)`` pools the first-frame-enhanced keys.  For
     fp8 codes (uint8) pass ``scales = (q_scale, k_scale)`` from the quantiser
-    (chorus_build_block_mask_fp8)."""
+    (chorus_build_block_mask_fp8).  ``kv_block`` = 64 or 128 tokens per kv
+    block (the mask's columns)."""
     L = load_library()
     if q.shape != k.shape or q.dtype != k.dtype:
         raise ValueError("q and k must share shape and dtype")
@@ -240,18 +247,20 @@ def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: 
         raise ValueError("scales are given exactly for fp8 codes")
     B, S, H, D = q.shape
     n = (S + BLOCK - 1) // BLOCK
+    nk = (S + kv_block - 1) // kv_block
     rows = B * H * n
     shape = _shape(q)
     sm = 1.0 / math.sqrt(D) if sm_scale is None else float(sm_scale)
     if out is None:
         out = BlockMask(torch.empty(rows + 1, dtype=torch.int32, device=q.device),
-                        torch.empty(rows * n, dtype=torch.int32, device=q.device), B, H, n)
-    if return_scores and out.block_scores is None:
-        out.block_scores = torch.empty((rows, n), dtype=torch.float32, device=q.device)
+                        torch.empty(rows * nk, dtype=torch.int32, device=q.device), B, H, n, kv_block)
+    out.block = kv_block
+    if return_scores and (out.block_scores is None or out.block_scores.shape != (rows, nk)):
+        out.block_scores = torch.empty((rows, nk), dtype=torch.float32, device=q.device)
     need = L.chorus_build_block_mask_workspace_size(ctypes.byref(shape))
     if workspace is None or workspace.numel() < need + 256:
         workspace = _workspace(need, q.device)
-    tail = (sm, float(top_p), float(min_top_k), _key_scale(key_scale), out.row_ptr.data_ptr(),
+    tail = (sm, float(top_p), float(min_top_k), int(kv_block), _key_scale(key_scale), out.row_ptr.data_ptr(),
             out.col_idx.data_ptr(), out.col_idx.numel(),
             _ptr(out.block_scores if return_scores else None), _aligned(workspace), need, _stream())
     if fp8:
@@ -367,10 +376,10 @@ def block_sparse_attn_fwd_fp8(q, k, v, q_scale, k_scale, v_scale, mask, **kw):
 
 
 def attn_block_mass(q: torch.Tensor, k: torch.Tensor, lse: torch.Tensor, sm_scale: float | None = None,
-                    out: torch.Tensor | None = None, key_scale=None) -> torch.Tensor:
-    """chorus_attn_block_mass: true block attention mass [B, H, n, n] (fp32)
-    of ``q, k [B, S, H, D]`` given the dense attention's ``lse [B, H, S]``
-    (computed with the same ``key_scale``)."""
+                    out: torch.Tensor | None = None, key_scale=None, kv_block: int = BLOCK) -> torch.Tensor:
+    """chorus_attn_block_mass: true block attention mass [B, H, n, n_kv]
+    (fp32) of ``q, k [B, S, H, D]`` given the dense attention's ``lse [B, H, S]``
+    (computed with the same ``key_scale``); kv blocks of ``kv_block`` tokens."""
     L = load_library()
     if q.shape != k.shape or q.dtype != k.dtype:
         raise ValueError("q and k must share shape and dtype")
@@ -379,33 +388,38 @@ def attn_block_mass(q: torch.Tensor, k: torch.Tensor, lse: torch.Tensor, sm_scal
     if lse.shape != (B, H, S) or lse.dtype != torch.float32 or not lse.is_contiguous():
         raise ValueError("lse must be a contiguous float32 [B, H, S] tensor")
     sm = (1.0 / math.sqrt(D)) if sm_scale is None else sm_scale
-    mass = out if out is not None else torch.empty((B, H, n, n), dtype=torch.float32, device=q.device)
-    if mass.shape != (B, H, n, n) or mass.dtype != torch.float32 or not mass.is_contiguous():
-        raise ValueError("out must be a contiguous float32 [B, H, n, n] tensor")
+    nk = (S + kv_block - 1) // kv_block
+    mass = out if out is not None else torch.empty((B, H, n, nk), dtype=torch.float32, device=q.device)
+    if mass.shape != (B, H, n, nk) or mass.dtype != torch.float32 or not mass.is_contiguous():
+        raise ValueError("out must be a contiguous float32 [B, H, n, n_kv] tensor")
     st = L.chorus_attn_block_mass(_dtype_code(q), ctypes.byref(_shape(q)), ctypes.byref(_tensor(q)),
-                                  ctypes.byref(_tensor(k)), lse.data_ptr(), sm, _key_scale(key_scale),
+                                  ctypes.byref(_tensor(k)), lse.data_ptr(), sm, int(kv_block),
+                                  _key_scale(key_scale),
                                   mass.data_ptr(), _stream())
     _check(st, "chorus_attn_block_mass")
     return mass
 
 
 def select_block_mask(mass: torch.Tensor, S: int, top_p: float, min_top_k: float,
-                      out: BlockMask | None = None, workspace: torch.Tensor | None = None) -> BlockMask:
+                      out: BlockMask | None = None, workspace: torch.Tensor | None = None,
+                      kv_block: int = BLOCK) -> BlockMask:
     """chorus_select_block_mask: CSR mask (mask_batch = B) cut from block
-    masses ``mass [B, H, n, n]`` of a sequence of S tokens."""
+    masses ``mass [B, H, n, n_kv]`` of a sequence of S tokens."""
     L = load_library()
-    B, H, n, n2 = mass.shape
-    if n != n2 or n != (S + 63) // 64 or mass.dtype != torch.float32 or not mass.is_contiguous():
-        raise ValueError("mass must be a contiguous float32 [B, H, n, n] tensor with n = ceil(S / 64)")
+    B, H, n, nk = mass.shape
+    if (n != (S + 63) // 64 or nk != (S + kv_block - 1) // kv_block or mass.dtype != torch.float32
+            or not mass.is_contiguous()):
+        raise ValueError("mass must be a contiguous float32 [B, H, ceil(S / 64), ceil(S / kv_block)] tensor")
     shape = Shape(B, S, H, 128)
     rows = B * H * n
     m = out if out is not None else BlockMask(
         torch.empty(rows + 1, dtype=torch.int32, device=mass.device),
-        torch.empty(rows * n, dtype=torch.int32, device=mass.device), B, H, n)
+        torch.empty(rows * nk, dtype=torch.int32, device=mass.device), B, H, n, kv_block)
+    m.block = kv_block
     need = L.chorus_select_block_mask_workspace_size(ctypes.byref(shape))
     ws = workspace if workspace is not None and workspace.numel() >= need + 256 else \
         _workspace(need, mass.device)
-    st = L.chorus_select_block_mask(ctypes.byref(shape), mass.data_ptr(), top_p, min_top_k,
+    st = L.chorus_select_block_mask(ctypes.byref(shape), mass.data_ptr(), int(kv_block), top_p, min_top_k,
                                     m.row_ptr.data_ptr(), m.col_idx.data_ptr(), m.col_idx.numel(),
                                     _aligned(ws), need, _stream())
     _check(st, "chorus_select_block_mask")
@@ -431,15 +445,20 @@ class VisitMap:
     """Device visited bitmap of a layer group (chorus_visit_*), sized for
     masks with the given mask_batch / H / n_blocks."""
 
-    def __init__(self, mask_batch: int, H: int, n_blocks: int, device="cuda"):
+    def __init__(self, mask_batch: int, H: int, n_blocks: int, device="cuda", block: int = BLOCK):
         L = load_library()
-        nbytes = L.chorus_visit_map_bytes(mask_batch, H, n_blocks)
-        self.mask_batch, self.H, self.n_blocks = mask_batch, H, n_blocks
-        self.words = (n_blocks + 31) // 32
+        desc = Mask(mask_batch, H, n_blocks, block, None, None)
+        nbytes = L.chorus_visit_map_bytes(ctypes.byref(desc))
+        if nbytes == 0:
+            raise ValueError("invalid mask description for a visited map")
+        self.mask_batch, self.H, self.n_blocks, self.block = mask_batch, H, n_blocks, block
+        self.n_kv = (n_blocks * BLOCK + block - 1) // block
+        self.words = (self.n_kv + 31) // 32
         self.bits = torch.empty(nbytes // 4, dtype=torch.int32, device=device)
 
     def _check_mask(self, mask: BlockMask):
-        if (mask.mask_batch, mask.H, mask.n_blocks) != (self.mask_batch, self.H, self.n_blocks):
+        if (mask.mask_batch, mask.H, mask.n_blocks, mask.block) != (self.mask_batch, self.H, self.n_blocks,
+                                                                    self.block):
             raise ValueError("mask dimensions differ from the visited map's")
 
     def reset(self, like: BlockMask):
@@ -458,10 +477,10 @@ class VisitMap:
         self._check_mask(mask)
         L = load_library()
         rows = mask.rows
-        n = mask.n_blocks
         m = out if out is not None else BlockMask(
             torch.empty(rows + 1, dtype=torch.int32, device=self.bits.device),
-            torch.empty(rows * n, dtype=torch.int32, device=self.bits.device), mask.mask_batch, mask.H, n)
+            torch.empty(rows * mask.n_kv, dtype=torch.int32, device=self.bits.device), mask.mask_batch, mask.H,
+            mask.n_blocks, mask.block)
         cm = mask.as_c()
         need = L.chorus_visit_refresh_workspace_size(ctypes.byref(cm))
         ws = workspace if workspace is not None and workspace.numel() >= need + 256 else \
@@ -476,4 +495,4 @@ class VisitMap:
         import numpy as np
         w = self.bits.cpu().numpy().view(np.uint32).reshape(-1, self.words)
         bits = ((w[:, :, None] >> np.arange(32, dtype=np.uint32)) & 1).astype(bool)
-        return bits.reshape(w.shape[0], -1)[:, : self.n_blocks]
+        return bits.reshape(w.shape[0], -1)[:, : self.n_kv]

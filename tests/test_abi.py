@@ -50,7 +50,7 @@ def shape(B=1, S=100, H=2, D=128):
     return ops.Shape(B, S, H, D)
 
 
-def build(lib, shp, q=None, top_p=0.5, mk=0.1, cap=None, ws_bytes=None, dtype=ops.BF16, ks=None):
+def build(lib, shp, q=None, top_p=0.5, mk=0.1, cap=None, ws_bytes=None, dtype=ops.BF16, ks=None, kvb=64):
     n = (shp.S + 63) // 64
     rows = shp.B * shp.H * n
     cap = rows * n if cap is None else cap
@@ -58,7 +58,7 @@ def build(lib, shp, q=None, top_p=0.5, mk=0.1, cap=None, ws_bytes=None, dtype=op
     ws = need if ws_bytes is None else ws_bytes
     qq = q or t4(shp.B, shp.S, shp.H)
     return lib.chorus_build_block_mask(dtype, ctypes.byref(shp), ctypes.byref(qq), ctypes.byref(qq),
-                                       0.088, top_p, mk, ks, FAKE, FAKE, cap, None, FAKE, ws, None)
+                                       0.088, top_p, mk, kvb, ks, FAKE, FAKE, cap, None, FAKE, ws, None)
 
 
 def test_builder_argument_checks(lib):
@@ -88,7 +88,8 @@ def attn(lib, shp, mask, dtype=ops.BF16, scales=(None, None, None), sched=None, 
 def test_attention_argument_checks(lib):
     shp = shape(B=2, S=100, H=2)
     ok = ops.Mask(1, 2, 2, 64, FAKE, FAKE)
-    assert attn(lib, shp, ops.Mask(1, 2, 2, 128, FAKE, FAKE)) == 2     # block 128
+    assert attn(lib, shp, ops.Mask(1, 2, 2, 256, FAKE, FAKE)) == 2     # kv block 256
+    assert attn(lib, shp, ops.Mask(1, 2, 2, 32, FAKE, FAKE)) == 2      # kv block 32
     assert attn(lib, shp, ops.Mask(3, 2, 2, 64, FAKE, FAKE)) == 1      # mask_batch
     assert attn(lib, shp, ops.Mask(1, 3, 2, 64, FAKE, FAKE)) == 1      # H
     assert attn(lib, shp, ops.Mask(1, 2, 3, 64, FAKE, FAKE)) == 1      # n_blocks
@@ -119,21 +120,21 @@ def test_block_mass_selection_and_coverage_check_arguments(lib):
     shp = shape(B=1, S=100, H=2)
     t = t4()
     assert lib.chorus_attn_block_mass(ops.FP8_E4M3, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
-                                      FAKE, 0.088, None, FAKE, None) == 2
+                                      FAKE, 0.088, 64, None, FAKE, None) == 2
     assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
-                                      None, 0.088, None, FAKE, None) == 1
+                                      None, 0.088, 64, None, FAKE, None) == 1
     assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
-                                      FAKE, -1.0, None, FAKE, None) == 1
+                                      FAKE, -1.0, 64, None, FAKE, None) == 1
     assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shape(D=64)), ctypes.byref(t), ctypes.byref(t),
-                                      FAKE, 0.088, None, FAKE, None) == 2
+                                      FAKE, 0.088, 64, None, FAKE, None) == 2
     need = lib.chorus_select_block_mask_workspace_size(ctypes.byref(shp))
     assert need > 0
     sel = lib.chorus_select_block_mask
-    assert sel(ctypes.byref(shp), FAKE, 1.5, 0.0, FAKE, FAKE, 8, FAKE, need, None) == 1
-    assert sel(ctypes.byref(shp), FAKE, 0.5, 0.0, FAKE, FAKE, 7, FAKE, need, None) == 3
-    assert sel(ctypes.byref(shp), FAKE, 0.5, 0.0, FAKE, FAKE, 8, FAKE, 16, None) == 5
-    assert sel(ctypes.byref(shp), None, 0.5, 0.0, FAKE, FAKE, 8, FAKE, need, None) == 1
-    assert sel(ctypes.byref(shape(S=64 * 4097)), FAKE, 0.5, 0.0, FAKE, FAKE, 1 << 40, FAKE, 1 << 40,
+    assert sel(ctypes.byref(shp), FAKE, 64, 1.5, 0.0, FAKE, FAKE, 8, FAKE, need, None) == 1
+    assert sel(ctypes.byref(shp), FAKE, 64, 0.5, 0.0, FAKE, FAKE, 7, FAKE, need, None) == 3
+    assert sel(ctypes.byref(shp), FAKE, 64, 0.5, 0.0, FAKE, FAKE, 8, FAKE, 16, None) == 5
+    assert sel(ctypes.byref(shp), None, 64, 0.5, 0.0, FAKE, FAKE, 8, FAKE, need, None) == 1
+    assert sel(ctypes.byref(shape(S=64 * 4097)), FAKE, 64, 0.5, 0.0, FAKE, FAKE, 1 << 40, FAKE, 1 << 40,
                None) == 2
     m = ops.Mask(1, 2, 2, 64, FAKE, FAKE)
     assert lib.chorus_mask_coverage(ctypes.byref(shp), ctypes.byref(m), None, FAKE, None) == 1
@@ -143,13 +144,17 @@ def test_block_mass_selection_and_coverage_check_arguments(lib):
 
 
 def test_visit_refresh_checks_arguments(lib):
-    assert lib.chorus_visit_map_bytes(1, 40, 1182) == 40 * 1182 * 37 * 4
-    assert lib.chorus_visit_map_bytes(0, 40, 1182) == 0
+    vb = lambda *a: lib.chorus_visit_map_bytes(ctypes.byref(ops.Mask(*a, None, None)))
+    assert vb(1, 40, 1182, 64) == 40 * 1182 * 37 * 4
+    assert vb(1, 40, 1182, 128) == 40 * 1182 * 19 * 4          # 591 kv blocks per row
+    assert vb(0, 40, 1182, 64) == 0
+    assert vb(1, 40, 1182, 96) == 0
+    assert lib.chorus_visit_map_bytes(None) == 0
     m = ops.Mask(1, 2, 10, 64, FAKE, FAKE)
     assert lib.chorus_visit_refresh_workspace_size(ctypes.byref(m)) >= 20 * 4 + 20 * 4
     assert lib.chorus_visit_reset(None, FAKE, None) == 1
     assert lib.chorus_visit_update(ctypes.byref(m), None, None) == 1
-    assert lib.chorus_visit_update(ctypes.byref(ops.Mask(1, 2, 10, 128, FAKE, FAKE)), FAKE, None) == 2
+    assert lib.chorus_visit_update(ctypes.byref(ops.Mask(1, 2, 10, 256, FAKE, FAKE)), FAKE, None) == 2
     assert lib.chorus_visit_update(ctypes.byref(ops.Mask(1, 2, 4097, 64, FAKE, FAKE)), FAKE, None) == 2
     assert lib.chorus_visit_update(ctypes.byref(ops.Mask(1, 2, 10, 64, None, FAKE)), FAKE, None) == 1
     need = lib.chorus_visit_refresh_workspace_size(ctypes.byref(m))
@@ -170,7 +175,7 @@ def test_key_scale_checks(lib):
         assert build(lib, shape(), ks=ks) == 1
         t = t4()
         assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shape(B=1, S=100, H=2)), ctypes.byref(t),
-                                          ctypes.byref(t), FAKE, 0.088, ks, FAKE, None) == 1
+                                          ctypes.byref(t), FAKE, 0.088, 64, ks, FAKE, None) == 1
     assert b"key_scale" in lib.chorus_last_error()
 
 
@@ -181,11 +186,27 @@ def test_fp8_builder_checks_arguments(lib):
     need = lib.chorus_build_block_mask_workspace_size(ctypes.byref(shp))
     t8 = ops.Tensor(FAKE, 100 * 2 * 128, 2 * 128, 128)
     f = lib.chorus_build_block_mask_fp8
-    assert f(ctypes.byref(shp), ctypes.byref(t8), None, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, None,
+    assert f(ctypes.byref(shp), ctypes.byref(t8), None, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, 64, None,
              FAKE, FAKE, cap, None, FAKE, need, None) == 1
-    assert f(ctypes.byref(shp), ctypes.byref(t8), FAKE, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, None,
+    assert f(ctypes.byref(shp), ctypes.byref(t8), FAKE, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, 64, None,
              FAKE, FAKE, cap - 1, None, FAKE, need, None) == 3
-    assert f(ctypes.byref(shape(D=64)), ctypes.byref(t8), FAKE, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, None,
+    assert f(ctypes.byref(shape(D=64)), ctypes.byref(t8), FAKE, ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, 64, None,
              FAKE, FAKE, cap, None, FAKE, need, None) == 2
     assert f(ctypes.byref(shp), ctypes.byref(ops.Tensor(FAKE + 4, 100 * 2 * 128, 2 * 128, 128)), FAKE,
-             ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, None, FAKE, FAKE, cap, None, FAKE, need, None) == 1
+             ctypes.byref(t8), FAKE, 0.088, 0.5, 0.1, 64, None, FAKE, FAKE, cap, None, FAKE, need, None) == 1
+
+
+def test_kv_block_checks(lib):
+    assert build(lib, shape(), kvb=96) == 2
+    assert build(lib, shape(), kvb=128) != 2 or b"kv_block" not in lib.chorus_last_error()
+    # kv blocks of 128: the worst-case capacity is rows * ceil(S / 128)
+    shp = shape(S=300)
+    rows = 1 * 2 * 5
+    assert build(lib, shp, kvb=128, cap=rows * 3 - 1) == 3
+    t = t4()
+    assert lib.chorus_attn_block_mass(ops.BF16, ctypes.byref(shape(B=1, S=100, H=2)), ctypes.byref(t),
+                                      ctypes.byref(t), FAKE, 0.088, 100, None, FAKE, None) == 2
+    need = lib.chorus_select_block_mask_workspace_size(ctypes.byref(shp))
+    assert lib.chorus_select_block_mask(ctypes.byref(shp), FAKE, 128, 0.5, 0.0, FAKE, FAKE, rows * 3 - 1,
+                                        FAKE, need, None) == 3
+    assert lib.chorus_validate_block_mask(ctypes.byref(ops.Mask(1, 2, 5, 100, FAKE, FAKE)), 10, FAKE, None) == 2
