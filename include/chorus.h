@@ -6,15 +6,24 @@
  * Image-to-Video Generation".  A block mask is built once (for a historical
  * request, Sec. 3.2 "Mask Caching and Retrieval") and then loaded and applied
  * as-is to the block-sparse attention of new, similar requests (same passage;
- * Sec. 3.2 Obs. 1).  This library provides the two pieces of that hot path:
+ * Sec. 3.2 Obs. 1).  This library provides the pieces of that hot path:
  *
  *   - the mask builder: mean-pooled block scores softmax(mean(Q) mean(K)^T)
  *     (Sec. 3.2 Obs. 2, the online predictor used on a cache miss) with joint
  *     top-p / minimum-top-k selection (Sec. 3.2 "Mask Caching and Retrieval",
- *     "Minimum top-k guarantee"; knobs top_p / min_top_k in Sec. 4.1);
- *   - the block-sparse attention forward pass that evaluates only the listed
- *     block pairs in QK^T, softmax and PV (Sec. 3.2 "Efficient block-sparse
- *     kernel"), in fp16/bf16 and in FP8 with fp32 accumulation.
+ *     "Minimum top-k guarantee"; knobs top_p / min_top_k in Sec. 4.1), its
+ *     work plan and a mask checker;
+ *   - the FP8 blockwise quantiser and the block-sparse attention forward
+ *     pass that evaluates only the listed block pairs in QK^T, softmax and
+ *     PV (Sec. 3.2 "Efficient block-sparse kernel"), in fp16/bf16 and in FP8
+ *     with fp32 accumulation;
+ *   - the true block attention mass of a historical request, the mask
+ *     selected from it, and the coverage of a mask (Sec. 3.2 "Mask Caching
+ *     and Retrieval", Obs. 1);
+ *   - block-pair visit refreshing over a layer group (Sec. 3.2 "Safety
+ *     fallback against information loss");
+ *   - the first-frame key enhancement of Eq. (1) (Sec. 3.4), applied on the
+ *     fly by the calls that take a key_scale.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -139,12 +148,13 @@ typedef struct {
  *      and writes them ascending as CSR row (b * H + h) * n_blocks + i.
  * The result has mask_batch = B and block = kv_block.  To build one mask from
  * one request (and reuse it for others), pass a B = 1 view of that request.
- * key_scale     : optional first-frame key enhancement (NULL for none): the
- *                 pooled keys are those of the scaled K.
  *
  * q, k          : [B, S, H, D] f16 or bf16 (dtype), read only.
- * row_ptr       : out, device int32 [B * H * n_blocks + 1].
+ * top_p, min_top_k : in [0, 1] (else CHORUS_ERR_INVALID_ARG).
  * kv_block      : 64 or 128 (else CHORUS_ERR_UNSUPPORTED).
+ * key_scale     : optional first-frame key enhancement (NULL for none): the
+ *                 pooled keys are those of the scaled K.
+ * row_ptr       : out, device int32 [B * H * n_blocks + 1].
  * col_idx       : out, device int32 [col_capacity]; col_capacity must be at
  *                 least B * H * n_blocks * n_kv (the worst case, since the
  *                 count is only known on device) else CHORUS_ERR_CAPACITY.
