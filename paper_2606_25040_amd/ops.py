@@ -333,11 +333,15 @@ def block_sparse_attn_fwd(q, k, v, mask: BlockMask | None, sm_scale: float | Non
     """
     L = load_library()
     dt = _dtype_code(q)
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise ValueError("q, k and v must share shape and dtype")
     B, S, H, D = q.shape
     sm = 1.0 / math.sqrt(D) if sm_scale is None else float(sm_scale)
+    odt = torch.bfloat16 if dt == FP8_E4M3 else q.dtype
     if out is None:
-        odt = torch.bfloat16 if dt == FP8_E4M3 else q.dtype
         out = torch.empty((B, S, H, D), dtype=odt, device=q.device)
+    elif out.shape != q.shape or out.dtype != odt:
+        raise ValueError(f"out must be a {odt} tensor of q's shape")
     lse = torch.empty((B, H, S), dtype=torch.float32, device=q.device) if return_lse else None
     qs = ks = vs = None
     if dt == FP8_E4M3:
