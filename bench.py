@@ -354,6 +354,20 @@ def main():
 
     reps = max(args.steps, 10)
     attn_ms = event_ms(lambda: attn(mask, sched), reps)
+
+    # per-launch spread of the attention kernel (one event pair per launch)
+    def launch_stats(fn, reps):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        ev[-1][1].synchronize()
+        t = sorted(a.elapsed_time(b) for a, b in ev)
+        return {"median": round(t[len(t) // 2], 4), "min": round(t[0], 4),
+                "p90": round(t[min(len(t) - 1, (9 * len(t)) // 10)], 4), "launches": len(t)}
+
+    attn_stats = launch_stats(lambda: attn(mask, sched), max(reps, 20))
     # the same launch with the first-frame key enhancement (first latent frame
     # = grid_y * grid_x tokens, beta 1.3)
     first_frame = wl.grid[1] * wl.grid[2]
@@ -416,6 +430,7 @@ def main():
             "step": "mask build + plan" + (" + fp8 quantise" if fp8 else "") + " + attention",
         },
         "attn_ms": round(attn_ms, 4),
+        "attn_ms_per_launch": attn_stats,
         "attn_tflops": round(attn_tflops, 2),
         "attn_frac_mfma_peak": round(attn_tflops / peak, 4),
         "attn_key_scaled_ms": round(attn_ks_ms, 4),
@@ -423,6 +438,13 @@ def main():
         "builder_fp8_input_ms": None if build_fp8_ms is None else round(build_fp8_ms, 4),
         "plan_ms": round(plan_ms, 4),
         "quant_ms": round(quant_ms, 4),
+        # HBM-bound stages: algorithmic bytes over time (the builder reads the
+        # mask source's Q and K once; the quantiser reads 2 B and writes 1 B per
+        # element of Q, K and V, plus the scales)
+        "builder_gbps": (round(2 * mq.numel() * mq.element_size() / (build_ms * 1e-3) / 1e9, 1)
+                         if mq is not None and build_ms > 0 else None),
+        "quant_gbps": (round((3 * 3 * q.numel() + 3 * 4 * B * H * n) / (quant_ms * 1e-3) / 1e9, 1)
+                       if fp8 and quant_ms > 0 else None),
         "visit_update_ms": round(visit_update_ms, 4),
         "visit_refresh_worst_ms": round(visit_refresh_ms, 4),
         "routing_overhead_ratio": round(build_ms / (build_ms + attn_ms), 4),
