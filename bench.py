@@ -48,6 +48,7 @@ def parse():
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--kv-block", type=int, default=64, choices=(64, 128),
                     help="tokens per kv block of the built mask (128 = the paper's kernel geometry)")
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay of the step")
     ap.add_argument("--f16", action="store_true",
                     help="run a 16-bit workload in f16 (its inputs converted) instead of bf16")
     ap.add_argument("--coverage", action="store_true",
@@ -327,6 +328,30 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
+
+    # the same step captured once into a HIP graph and replayed (the path
+    # allocates nothing and records no memset nodes), reported beside the
+    # eager step
+    graph_ms = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        graph_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        del graph
     mask = build()
     sched = plan(mask)
     torch.cuda.synchronize()
@@ -416,6 +441,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -1,0 +1,97 @@
+"""The whole hot path captured into a HIP graph (torch.cuda.CUDAGraph) and
+replayed: mask build, plan, fp8 quantisation and attention allocate nothing
+and use no memset nodes, so a captured step must reproduce the eager step
+bit for bit on every replay, with unrelated eager work between replays."""
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_25040_amd import ops
+from paper_2606_25040_amd import workloads as wk
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def device():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    ops.load_library()
+    torch.cuda.set_device(0)
+    yield
+
+
+class Step:
+    """Preallocated buffers of one step: build + plan (+ quantise) + attention."""
+
+    def __init__(self, q, k, v, top_p, mk, sm, fp8, kv_block=64):
+        B, S, H, D = q.shape
+        n = (S + 63) // 64
+        nk = (S + kv_block - 1) // kv_block
+        self.q, self.k, self.v, self.top_p, self.mk, self.sm, self.fp8 = q, k, v, top_p, mk, sm, fp8
+        self.kv_block = kv_block
+        self.mask = ops.BlockMask(torch.empty(B * H * n + 1, dtype=torch.int32, device="cuda"),
+                                  torch.empty(B * H * n * nk, dtype=torch.int32, device="cuda"), B, H, n, kv_block)
+        need = ops.load_library().chorus_build_block_mask_workspace_size(ops.ctypes.byref(ops._shape(q)))
+        self.ws = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
+        self.order = torch.empty(B * H, dtype=torch.int32, device="cuda")
+        self.out = torch.empty((B, S, H, D), dtype=torch.bfloat16 if fp8 else q.dtype, device="cuda")
+        if fp8:
+            self.codes = [torch.empty((B, S, H, D), dtype=torch.uint8, device="cuda") for _ in range(3)]
+            self.scales = [torch.empty((B, H, n), dtype=torch.float32, device="cuda") for _ in range(3)]
+
+    def __call__(self):
+        m = ops.build_block_mask(self.q, self.k, self.top_p, self.mk, sm_scale=self.sm, out=self.mask,
+                                 workspace=self.ws, kv_block=self.kv_block)
+        ops.plan_block_mask(m, self.q.shape[0], self.q.shape[1], out=self.order)
+        if self.fp8:
+            for x, c, s in zip((self.q, self.k, self.v), self.codes, self.scales):
+                ops.quantize_fp8_blockwise(x, codes=c, scales=s)
+            ops.block_sparse_attn_fwd(*self.codes, m, sm_scale=self.sm, scales=tuple(self.scales), out=self.out,
+                                      schedule=self.order)
+        else:
+            ops.block_sparse_attn_fwd(self.q, self.k, self.v, m, sm_scale=self.sm, out=self.out,
+                                      schedule=self.order)
+
+    def snapshot(self):
+        rp, ci = self.mask.to_host()
+        snap = [rp, ci, self.order.cpu().numpy(), self.out.view(torch.int16).cpu().numpy()]
+        if self.fp8:
+            snap += [c.cpu().numpy() for c in self.codes] + [s.cpu().numpy() for s in self.scales]
+        return snap
+
+
+@pytest.mark.parametrize("fp8,kv_block", [(False, 64), (True, 64), (False, 128)])
+def test_captured_step_replays_match_eager(fp8, kv_block):
+    gen = torch.Generator().manual_seed(11)
+    B, S, H = 1, 3000, 4
+    q, k, v = ((torch.randn(B, S, H, 128, generator=gen) * s).to(torch.bfloat16).cuda() for s in (0.5, 0.5, 1.0))
+    step = Step(q, k, v, 0.8, 0.05, 128 ** -0.5, fp8, kv_block)
+    step()
+    torch.cuda.synchronize()
+    ref = step.snapshot()
+
+    # other eager work on the same library between replays: a second step on
+    # other inputs, writing its own buffers
+    q2, k2, v2 = (x.flip(1).contiguous() for x in (q, k, v))
+    other = Step(q2, k2, v2, 0.5, 0.1, 128 ** -0.5, fp8, kv_block)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()                                   # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(3):
+        for t in [step.out] + [step.order] + ([*step.codes] if fp8 else []):
+            t.zero_()
+        step.mask.col_idx.fill_(-7)
+        graph.replay()
+        other()
+        torch.cuda.synchronize()
+        got = step.snapshot()
+        for a, b in zip(got, ref):
+            assert np.array_equal(a, b), f"replay {rep} differs"
