@@ -232,7 +232,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(this build measures the single-GPU share of the path).", file=sys.stderr)
+              "(what is measured is the single-GPU share of the path).", file=sys.stderr)
         sys.exit(2)
     if args.coverage:
         coverage_study(args)
