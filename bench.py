@@ -79,12 +79,17 @@ def traffic_from_profile(kernel_file: str, workload: str, src_hash: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, inp, budget_s: float):
+def cpu_baseline(wl, inp, budget_s: float, gpu=None):
     """Oracle (plain NumPy float64) on a bounded sample of the same workload:
     head by head of request 0, the oracle mask builder for the head (or the
     fixed mask's rows) followed by the oracle attention of that head's
     q-blocks in order, until about ``budget_s`` seconds of work are spent.
-    Returns effective TFLOP/s on computed blocks and a description."""
+    Returns effective TFLOP/s on computed blocks and a description.
+
+    With ``gpu = (row_ptr, col_idx, out)`` (the GPU mask of request 0 and the
+    GPU attention output), every sampled q-block whose GPU mask row equals the
+    oracle's is also compared with the GPU output (outside the timed work);
+    the statistics are returned as a second value."""
     from oracle import attention as oa
     from oracle import mask as om
     try:
@@ -97,6 +102,7 @@ def cpu_baseline(wl, inp, budget_s: float):
     pairs = 0
     blocks_done = 0
     heads_done = 0
+    cmp = {"q_blocks": 0, "rows_differing": 0, "max_abs": 0.0, "sum_abs": 0.0, "n": 0, "d2": 0.0, "r2": 0.0}
     for h in range(wl.H):
         t0 = time.perf_counter()
         if inp.mask_q is not None:
@@ -114,16 +120,32 @@ def cpu_baseline(wl, inp, budget_s: float):
                           [0, :, 0] for x in (inp.q, inp.k, inp.v))
         else:
             qh, kh, vh = (x[0, :, h].float().numpy() for x in (inp.q, inp.k, inp.v))
+        oh = None if gpu is None else gpu[2][0, :, h].float().cpu().numpy().astype(np.float64)
         t1 = time.perf_counter()
         t_build += t1 - t0
         done = 0
+        t_cmp = 0.0
         for i in range(wl.n_blocks):
-            oa.attention_block(qh, kh, vh, rows[i], i, wl.sm_scale)
+            o_i, _ = oa.attention_block(qh, kh, vh, rows[i], i, wl.sm_scale)
             pairs += len(rows[i])
             done += 1
-            if t_build + t_attn + (time.perf_counter() - t1) > budget_s:
+            if gpu is not None:
+                tc = time.perf_counter()
+                r = h * wl.n_blocks + i
+                if np.array_equal(np.asarray(gpu[1][gpu[0][r]:gpu[0][r + 1]]), np.asarray(rows[i])):
+                    d = np.abs(oh[i * 64:i * 64 + o_i.shape[0]] - o_i)
+                    cmp["q_blocks"] += 1
+                    cmp["max_abs"] = max(cmp["max_abs"], float(d.max()))
+                    cmp["sum_abs"] += float(d.sum())
+                    cmp["n"] += d.size
+                    cmp["d2"] += float((d * d).sum())
+                    cmp["r2"] += float((o_i * o_i).sum())
+                else:
+                    cmp["rows_differing"] += 1
+                t_cmp += time.perf_counter() - tc
+            if t_build + t_attn + (time.perf_counter() - t1 - t_cmp) > budget_s:
                 break
-        t_attn += time.perf_counter() - t1
+        t_attn += time.perf_counter() - t1 - t_cmp
         blocks_done += done
         heads_done += 1
         if t_build + t_attn > budget_s:
@@ -132,8 +154,15 @@ def cpu_baseline(wl, inp, budget_s: float):
     sample = (f"request 0, heads 0..{heads_done - 1}: oracle mask builder per head ({t_build:.2f} s incl. "
               f"input casts) + oracle attention (gather form, float64) of {blocks_done} q-blocks in order "
               f"({pairs} computed block pairs, {t_attn:.2f} s); float64 NumPy, BLAS threads {threads}")
-    return {"value": value, "unit": "TFLOP/s", "cores": min(threads, cores), "kind": "oracle",
+    base = {"value": value, "unit": "TFLOP/s", "cores": min(threads, cores), "kind": "oracle",
             "sample": sample}
+    if gpu is None:
+        return base, None
+    par = {"q_blocks_compared": cmp["q_blocks"], "q_blocks_with_differing_mask_row": cmp["rows_differing"],
+           "max_abs_err": cmp["max_abs"], "mean_abs_err": cmp["sum_abs"] / max(cmp["n"], 1),
+           "rel_frobenius_err": (cmp["d2"] / cmp["r2"]) ** 0.5 if cmp["r2"] > 0 else None,
+           "reference": "oracle (float64) on the cpu_baseline sample, where its mask row equals the GPU's"}
+    return base, par
 
 
 def coverage_study(args) -> None:
@@ -491,7 +520,12 @@ def main():
         },
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, inp, args.cpu_budget)
+        attn(mask, sched)                # the step's attention output again (later runs overwrote it)
+        torch.cuda.synchronize()
+        grp, gci = mask.to_host()
+        # (the oracle sample follows the kv-64 geometry; with --kv-block 128 no rows are compared)
+        gpu = (grp, gci, out) if kvb == 64 else None
+        line["cpu_baseline"], line["parity_sample"] = cpu_baseline(wl, inp, args.cpu_budget, gpu)
     print(json.dumps(line), flush=True)
 
 

@@ -448,3 +448,24 @@ def test_full_size_attention_sampled(key):
             o_ref, _ = oa.attention_block(qh, kh, vh, oa.row_blocks(rp, ci, r), i, wl.sm_scale)
             worst = max(worst, max_abs_err(oh[i * 64:i * 64 + o_ref.shape[0]], o_ref))
     assert worst <= tol, worst
+
+
+def test_plan_beyond_4096_units_keeps_natural_order_and_results():
+    """B * H > 4096 units: the plan keeps the natural order; any order gives
+    bitwise the same attention output."""
+    B, H, S = 65, 64, 64
+    n = 1
+    rng = np.random.Generator(np.random.PCG64(4097))
+    rp = np.arange(B * H * n + 1, dtype=np.int64)
+    ci = np.zeros(B * H * n, dtype=np.int64)
+    mask = ops.BlockMask.from_host(rp, ci, B, H, n)
+    order = ops.plan_block_mask(mask, B, S)
+    assert order.cpu().tolist() == list(range(B * H))
+    gen = torch.Generator().manual_seed(2)
+    q, k, v = rand_qkv(gen, B, S, H, torch.bfloat16)
+    q, k, v = q.cuda(), k.cuda(), v.cuda()
+    ref = ops.block_sparse_attn_fwd(q, k, v, mask)
+    perm = torch.from_numpy(rng.permutation(B * H).astype(np.int32)).cuda()
+    out = ops.block_sparse_attn_fwd(q, k, v, mask, schedule=perm)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
