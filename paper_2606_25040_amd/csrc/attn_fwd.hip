@@ -22,6 +22,11 @@
 // global addresses instead of the LDS ones) so that the b128 K reads and the
 // transposed b64 V reads are bank-conflict free.
 // Epilogue: O = O^T / l written as 16-bit, lse = ln(sum exp) in fp32.
+// Template flags: DENSE walks every kv block (no mask); KSCALE multiplies the
+// logits of keys below n_first by beta (first-frame key enhancement, Eq. 1);
+// KV2 reads a mask of 128-token kv blocks and walks each as its two 64-token
+// halves.  Each flag is its own instantiation, so the plain path carries none
+// of the others' work.
 #include "attn_common.h"
 
 namespace chorus {

@@ -21,6 +21,9 @@
 //   * the running max moves only when a row max grew by more than
 //     kRescaleLog2, which keeps P~ <= 2^(kPShift + kRescaleLog2) < 448.
 // P~ never leaves registers.
+// Template flags as in the 16-bit kernel: DENSE (no mask), KSCALE (Eq. 1
+// first-frame key enhancement on the dequantised keys), KV2 (kv blocks of 128
+// tokens walked as their 64-token halves).
 #include "attn_common.h"
 
 namespace chorus {
