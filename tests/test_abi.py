@@ -210,3 +210,22 @@ def test_kv_block_checks(lib):
     assert lib.chorus_select_block_mask(ctypes.byref(shp), FAKE, 128, 0.5, 0.0, FAKE, FAKE, rows * 3 - 1,
                                         FAKE, need, None) == 3
     assert lib.chorus_validate_block_mask(ctypes.byref(ops.Mask(1, 2, 5, 100, FAKE, FAKE)), 10, FAKE, None) == 2
+
+
+def test_header_is_plain_c_and_a_c_caller_links(tmp_path):
+    """Compile a C99 caller against include/chorus.h with gcc and run it:
+    host-side calls only (argument validation, sizes, strings)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    exe = tmp_path / "abi_c_caller"
+    lib_dir = os.path.dirname(ops.LIB_PATH)
+    cmd = [gcc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-I", os.path.join(ROOT, "include"),
+           os.path.join(ROOT, "tests", "abi_c_caller.c"), "-L", lib_dir, "-lchorus",
+           f"-Wl,-rpath,{lib_dir}", "-o", str(exe)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok"), r.stdout + r.stderr
