@@ -15,8 +15,14 @@ in fp32.  For one block X of up to 64 x D values:
     code  = e4m3fn_rne(clamp(y, -448, 448))
     scale = fp32(amax / 448)
 
-amax == 0 gives inv = 0 (codes encode +-0) and scale = 1.  The dequantised
-value the FP8 attention consumes is code_value * scale (exact in float64).
+amax == 0 gives inv = 0 (codes encode +-0) and scale = 1.  In a block with
+0 < amax < 2^-64, x and amax are first multiplied by 2^64 (exact for 16-bit
+inputs): the codes depend on x / amax only, so the scaled form gives the same
+codes wherever the plain one is finite, and it keeps 448 / amax finite below
+448 / FLT_MAX, where the plain fp32 reciprocal overflows.
+The scale stays fp32(amax / 448) of the unscaled amax (subnormal for such
+blocks).  The dequantised value the FP8 attention consumes is
+code_value * scale (exact in float64).
 """
 
 from __future__ import annotations
@@ -81,13 +87,14 @@ def quantize_block(xb) -> tuple[np.ndarray, np.float32]:
     """Quantise one block (any shape) following the module docstring."""
     xb = np.asarray(xb, dtype=np.float32)
     amax = np.float32(np.max(np.abs(xb))) if xb.size else np.float32(0)
+    up = np.float32(2.0 ** 64) if 0 < amax < np.float32(2.0 ** -64) else np.float32(1.0)
     if amax == 0:
         inv = np.float32(0.0)
         scale = np.float32(1.0)
     else:
-        inv = np.float32(np.float32(E4M3_MAX) / amax)
+        inv = np.float32(np.float32(E4M3_MAX) / np.float32(amax * up))
         scale = np.float32(amax / np.float32(E4M3_MAX))
-    y = (xb * inv).astype(np.float32)
+    y = ((xb * up).astype(np.float32) * inv).astype(np.float32)
     y = np.clip(y, np.float32(-E4M3_MAX), np.float32(E4M3_MAX))
     return encode_rne(y), scale
 

@@ -46,21 +46,44 @@ __device__ inline int v8_swz(int r, int c) { return c ^ (2 * ((r >> 1) & 3)); }
 
 // This wave's share of one 64 x 128 code tile: instruction u (0, 1) fills LDS
 // rows 8 (4u + wave) .. + 7 (1 KB, lane-linear: lane -> row + lane / 8,
-// chunk lane % 8); K rows fetch the permuted key.  Rows past the sequence
-// end re-read token S - 1 (masked keys, zero probabilities).
+// chunk lane % 8); K rows fetch the permuted key.  Full blocks take the row
+// offset from the scalar base and a per-lane offset fixed for the whole
+// kernel; rows of a partial last block past the sequence end re-read token
+// S - 1 (masked keys, zero probabilities).
 template <bool IS_K>
-__device__ inline void load_tile8(uint32_t lds, const char* base, uint32_t ss, int j, int S, int wave,
-                                  int lane) {
+struct Tile8Loader {
+  const char* base;
+  uint32_t ss;
+  uint32_t off[2];
+  __device__ void init(const char* b, uint32_t s, int wave, int lane) {
+    base = b;
+    ss = s;
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int r = 8 * (4 * u + wave) + (lane >> 3);
-    const int p = lane & 7;
-    const int c = IS_K ? k8_swz(r, p) : v8_swz(r, p);
-    const int key = IS_K ? k_key_of_row(r) : r;
-    const int tok = min(j * kBlock + key, S - 1);
-    dma16(lds + (4 * u + wave) * 1024, base, (uint32_t)tok * ss + (uint32_t)c * 16);
+    for (int u = 0; u < 2; ++u) off[u] = (uint32_t)key(u, wave, lane) * ss + (uint32_t)chunk(u, wave, lane) * 16;
   }
-}
+  static __device__ int row(int u, int wave, int lane) { return 8 * (4 * u + wave) + (lane >> 3); }
+  static __device__ int chunk(int u, int wave, int lane) {
+    const int r = row(u, wave, lane), p = lane & 7;
+    return IS_K ? k8_swz(r, p) : v8_swz(r, p);
+  }
+  static __device__ int key(int u, int wave, int lane) {
+    const int r = row(u, wave, lane);
+    return IS_K ? k_key_of_row(r) : r;
+  }
+  __device__ void load(uint32_t lds, int j, int S, int wave, int lane) const {
+    if (j * kBlock + kBlock <= S) {
+      const char* rowj = base + (int64_t)j * kBlock * ss;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) dma16(lds + (4 * u + wave) * 1024, rowj, off[u]);
+    } else {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int tok = min(j * kBlock + key(u, wave, lane), S - 1);
+        dma16(lds + (4 * u + wave) * 1024, base, (uint32_t)tok * ss + (uint32_t)chunk(u, wave, lane) * 16);
+      }
+    }
+  }
+};
 
 template <bool DENSE, bool KSCALE, bool KV2>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
@@ -103,18 +126,22 @@ void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
     __syncthreads();
     sref = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   }
-  const float log2_sref = __builtin_log2f(sref > 0.f ? sref : 1.f);
+  constexpr float kMinNormal = 1.17549435e-38f;
+  const float log2_sref = __builtin_log2f(sref > 0.f ? fmaxf(sref, kMinNormal) : 1.f);
 
   const char* kbase = static_cast<const char*>(a.k.data) + (int64_t)b * a.k.sb + (int64_t)h * a.k.sh;
   const char* vbase = static_cast<const char*>(a.v.data) + (int64_t)b * a.v.sb + (int64_t)h * a.v.sh;
-  const uint32_t kss = (uint32_t)a.k.ss, vss = (uint32_t)a.v.ss;
+  Tile8Loader<true> kl;
+  Tile8Loader<false> vl;
+  kl.init(kbase, (uint32_t)a.k.ss, wave, lane);
+  vl.init(vbase, (uint32_t)a.v.ss, wave, lane);
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)&tiles[0][0][0];
 
   bool in_a, in_b;
   int j = walk.next(in_a, in_b);
   if (j != INT32_MAX) {
-    load_tile8<true>(lds0, kbase, kss, j, S, wave, lane);
-    load_tile8<false>(lds0 + kTile8, vbase, vss, j, S, wave, lane);
+    kl.load(lds0, j, S, wave, lane);
+    vl.load(lds0 + kTile8, j, S, wave, lane);
   }
 
   // Q^T fragments (codes): query qrow, head-dim bytes 64 s + 32 hl .. + 32
@@ -159,8 +186,8 @@ void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
     __syncthreads();
     if (jn != INT32_MAX) {
       const uint32_t nxt = lds0 + (buf ^ 1) * 2 * kTile8;
-      load_tile8<true>(nxt, kbase, kss, jn, S, wave, lane);
-      load_tile8<false>(nxt + kTile8, vbase, vss, jn, S, wave, lane);
+      kl.load(nxt, jn, S, wave, lane);
+      vl.load(nxt + kTile8, jn, S, wave, lane);
     }
     if (mine && q_active) {
       const uint8_t* k_s = &tiles[buf][0][0];
@@ -216,7 +243,9 @@ void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[u][r] *= alpha;
       }
-      const float bias = __builtin_log2f(vsc[j]) - log2_sref + kPShift;   // log2(2^kPShift f_j)
+      // log2(2^kPShift f_j); both scales are clamped to the smallest normal
+      // float (the raw v_log_f32 takes no denormals), so f_j <= 1 still holds
+      const float bias = __builtin_amdgcn_logf(fmaxf(vsc[j], kMinNormal)) - log2_sref + kPShift;
       const float mb = m_run - bias;
       float rs = 0.f;
       i32x8 pw;

@@ -3,6 +3,9 @@
 // high-precision accumulation).  One scale per (request, head, 64-token block):
 //   amax = max|x|, inv = 448 / amax (IEEE fp32 divide), code = e4m3fn RNE of
 //   clamp(x * inv, -448, 448), scale = amax / 448; amax == 0 -> inv 0, scale 1.
+//   Blocks with amax < 2^-64 take x and amax times 2^64 (exact) before the
+//   reciprocal, which would overflow below 448 / FLT_MAX; the codes depend on
+//   x / amax only, so every other block is unchanged.
 // HBM-bound: each value is read once (2 bytes) and written once (1 byte).
 #include "chorus_internal.h"
 
@@ -51,7 +54,8 @@ __global__ __launch_bounds__(256) void quant_fp8_kernel(TensorArg x, TensorArg c
   if ((tid & 63) == 0) red[tid >> 6] = amax;
   __syncthreads();
   amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  const float inv = amax > 0.f ? 448.f / amax : 0.f;
+  const float up = amax < 0x1p-64f ? 0x1p64f : 1.f;
+  const float inv = amax > 0.f ? 448.f / (amax * up) : 0.f;
   if (tid == 0) scales[((int64_t)b * H + h) * n + blk] = amax > 0.f ? amax / 448.f : 1.f;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
@@ -62,7 +66,7 @@ __global__ __launch_bounds__(256) void quant_fp8_kernel(TensorArg x, TensorArg c
     for (int hw = 0; hw < 2; ++hw) {
       float y[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) y[e] = fminf(fmaxf(v[u][4 * hw + e] * inv, -448.f), 448.f);
+      for (int e = 0; e < 4; ++e) y[e] = fminf(fmaxf((v[u][4 * hw + e] * up) * inv, -448.f), 448.f);
       int word = __builtin_amdgcn_cvt_pk_fp8_f32(y[0], y[1], 0, false);
       word = __builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], word, true);
       packed[hw] = word;

@@ -85,6 +85,10 @@ def test_quantizer_bit_exact(dtype):
     x[1, 128:192, 0] = -0.0
     x[1, 192:256, 2] *= 1e-3                               # values deep in the subnormal range
     x[0, 960:, 2] = 1e4 if dtype == torch.bfloat16 else 6e4
+    if dtype == torch.bfloat16:
+        # amax below 448 / FLT_MAX (the reciprocal is taken after a 2^64
+        # pre-scale), with fp32-subnormal inputs and a subnormal scale
+        x[1, 320:384, 1] *= 2.0 ** -123
     x = x.to(dtype)
     codes, scales = ops.quantize_fp8_blockwise(x.cuda())
     torch.cuda.synchronize()
@@ -328,6 +332,38 @@ def test_attention_fp8_small_full():
     assert np.array_equal(np.isfinite(lg), fin)
     if fin.any():
         assert np.max(np.abs(lg[fin] - L[fin])) <= 1e-3
+
+
+def test_attention_fp8_extreme_value_block_scales():
+    """V blocks whose fp8 scale is zero-input (scale 1), denormal (values of
+    order 1e-37) or large sit next to ordinary blocks in the same rows: the
+    per-block V scale folded into the exponent stays finite and the output
+    matches the oracle on the dequantised inputs."""
+    gen = torch.Generator().manual_seed(33)
+    B, S, H = 1, 640, 2
+    q, k, v = rand_qkv(gen, B, S, H, torch.bfloat16)
+    n = S // 64
+    v = v.float()
+    v[:, 64:128] = 0.0                      # all-zero block: scale 1, codes 0
+    v[:, 192:256] *= 1e-36                  # subnormal block scale (amax / 448 < FLT_MIN)
+    v[:, 448:512] *= 2.0 ** -123            # amax below 448 / FLT_MAX
+    v[:, 320:384] *= 3e3                    # large block next to unit ones
+    v = v.to(torch.bfloat16)
+    rp = np.arange(0, H * n * n + 1, n)
+    ci = np.tile(np.arange(n), H * n)
+    mask = ops.BlockMask.from_host(rp, ci, 1, H, n)
+    (qc, qs), (kc, ks), (vc, vs) = (ops.quantize_fp8_blockwise(x.cuda()) for x in (q, k, v))
+    assert float(vs[0, 0, 3].item()) < 1.17549435e-38   # the denormal case is present
+    out = ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs))
+    torch.cuda.synchronize()
+    got = np64(out)
+    assert np.all(np.isfinite(got))
+    deq = [of.dequantize_blockwise(c.cpu().numpy(), s_.cpu().numpy()) for c, s_ in ((qc, qs), (kc, ks), (vc, vs))]
+    O, _ = oa.attention(*deq, rp, ci, 1.0 / math.sqrt(128), 1)
+    # fp8 P~ (relative 2^-4 per weight) on values up to 3e3 in magnitude
+    Oabs, _ = oa.attention(deq[0], deq[1], np.abs(deq[2]), rp, ci, 1.0 / math.sqrt(128), 1)
+    bound = np.maximum(TOL8, 1e-3 + 2.0 ** -4 * Oabs) + 2.0 ** -8 * np.abs(O)
+    assert np.all(np.abs(got - O) <= bound), float(np.max(np.abs(got - O) - bound))
 
 
 # --------------------------------------------------------------------------- mask checker

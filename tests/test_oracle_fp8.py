@@ -6,6 +6,7 @@ nearest-value search over the decode table, and the format's error bound.
 """
 
 import numpy as np
+import pytest
 import torch
 
 from oracle import fp8 as of
@@ -130,3 +131,28 @@ def test_quantize_scale_is_correctly_rounded(rng):
         exact = float(np.max(np.abs(x.astype(np.float64)))) / 448.0
         half_ulp = np.spacing(np.float32(scale)) / 2
         assert abs(float(scale) - exact) <= half_ulp
+
+
+@pytest.mark.parametrize("k", [0, 40, 70, 123])
+def test_quantize_codes_are_invariant_under_power_of_two_scaling(rng, k):
+    """The codes depend on x / amax only: a block scaled by 2^-k (exactly
+    representable in bf16 down to 2^-126) gets the codes of the
+    unscaled block and a scale 2^-k times its scale (the nearest fp32 to
+    amax / 448 once that is subnormal), including blocks below
+    amax = 448 / FLT_MAX ~ 1.3e-36, where a plain fp32 448 / amax overflows."""
+    x = (rng.standard_normal((64, 128)) * 2.0).astype(np.float32)
+    x = np.where(np.abs(x) < 2.0 ** -3, np.float32(2.0 ** -3), x)
+    x = torch.from_numpy(x).to(torch.bfloat16).float().numpy()
+    c0, s0 = of.quantize_block(x)
+    xs = (x.astype(np.float64) * 2.0 ** -k).astype(np.float32)
+    assert np.array_equal(xs.astype(np.float64) * 2.0 ** k, x.astype(np.float64))   # exact scaling
+    c1, s1 = of.quantize_block(xs)
+    assert np.array_equal(c1, c0)
+    exact = float(np.max(np.abs(xs))) / 448.0
+    if exact >= float(np.finfo(np.float32).tiny):
+        assert np.float64(s1) == np.float64(s0) * 2.0 ** -k
+    else:
+        # subnormal scale: still the nearest fp32 to amax / 448
+        assert abs(float(s1) - exact) <= 2.0 ** -150
+    if k >= 123:
+        assert float(np.max(np.abs(xs))) < 448.0 / float(np.finfo(np.float32).max)
