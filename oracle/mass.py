@@ -80,11 +80,13 @@ def block_mass_all(q, k, sm_scale: float, block: int = BLOCK, kv_block: int | No
 def select_row_from_mass(m_row, top_p: float, min_top_k: float) -> np.ndarray:
     """One mask row from block masses: order (mass desc, index asc), the
     smallest prefix whose share of the row's mass reaches top_p, the top-k
-    floor, at least one block; ids ascending."""
+    floor, at least one block; ids ascending.  A row of zero total mass has
+    zero shares, so a top_p > 0 is never reached and every block is kept."""
     m_row = np.asarray(m_row, dtype=np.float64)
     n = m_row.shape[0]
     order = np.lexsort((np.arange(n), -m_row))
-    share = m_row[order] / m_row.sum()
+    total = m_row.sum()
+    share = m_row[order] / total if total > 0 else np.zeros(n)
     kp = om.top_p_count(share, top_p)
     k = min(n, max(kp, om.floor_count(min_top_k, n), 1))
     return np.sort(order[:k])
