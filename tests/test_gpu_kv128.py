@@ -103,6 +103,35 @@ def test_attention_kv128_matches_oracle(dtype, S, B, H):
     assert torch.equal(out.view(torch.int16), out64.view(torch.int16))
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
+@pytest.mark.parametrize("S,n_first,beta", [(1090, 300, 1.6), (1000, 1000, 0.8)])
+def test_attention_kv128_key_scale_per_request_masks(dtype, S, n_first, beta):
+    """kv blocks of 128 with the first-frame key enhancement and one mask per
+    request (mask_batch = B): the KSCALE x KV2 instantiation of the 16-bit
+    kernel against the oracle on explicitly scaled keys."""
+    B, H = 2, 2
+    q, k, v = rand_qkv(S + n_first, B, S, H, dtype)
+    n, nk = (S + 63) // 64, (S + 127) // 128
+    rng = np.random.Generator(np.random.PCG64(n_first))
+    rp, ci = wk.random_csr(rng, B * H * n, nk, 0.4, empty_frac=0.1)
+    mask = ops.BlockMask.from_host(rp, ci, B, H, n, block=128)
+    sm = 1.0 / math.sqrt(128)
+    out, lse = ops.block_sparse_attn_fwd(q.cuda(), k.cuda(), v.cuda(), mask, sm_scale=sm, return_lse=True,
+                                         key_scale=(n_first, beta))
+    torch.cuda.synchronize()
+    ke = og.enhance_first_frame_keys(np64(k), n_first, beta)
+    O, L = oa.attention(np64(q), ke, np64(v), rp, ci, sm, B, kv_block=128)
+    assert within(np64(out), O, dtype, TOL16), float(np.max(np.abs(np64(out) - O)))
+    lg = lse.cpu().numpy()
+    fin = np.isfinite(L)
+    assert np.array_equal(np.isfinite(lg), fin)
+    assert np.max(np.abs(lg[fin] - L[fin])) <= 1e-3
+    erp, eci = expand(rp, ci, n)
+    out64 = ops.block_sparse_attn_fwd(q.cuda(), k.cuda(), v.cuda(), ops.BlockMask.from_host(erp, eci, B, H, n),
+                                      sm_scale=sm, key_scale=(n_first, beta))
+    assert torch.equal(out.view(torch.int16), out64.view(torch.int16))
+
+
 @pytest.mark.parametrize("S", [1000, 960])
 def test_attention_fp8_kv128(S):
     B, H = 2, 2

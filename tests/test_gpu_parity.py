@@ -14,6 +14,7 @@ import torch
 
 from oracle import attention as oa
 from oracle import fp8 as of
+from oracle import guidance as og
 from oracle import mask as om
 from paper_2606_25040_amd import ops
 from paper_2606_25040_amd import workloads as wk
@@ -251,6 +252,37 @@ def test_attention_full_density_equals_dense_sdpa():
         q.double().permute(0, 2, 1, 3), k.double().permute(0, 2, 1, 3),
         v.double().permute(0, 2, 1, 3)).permute(0, 2, 1, 3)
     assert within_rounding(np64(out), ref.numpy(), torch.bfloat16)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "fp8"])
+@pytest.mark.parametrize("key_scale", [None, (400, 1.5)])
+def test_attention_without_mask_is_the_full_density_mask(dtype, key_scale):
+    """mask = NULL (every kv block, the dense instantiations) gives bitwise the
+    output of an explicit full-density mask, and that matches the oracle."""
+    gen = torch.Generator().manual_seed(5)
+    B, S, H = 2, 700, 2
+    tdt = torch.float16 if dtype == "f16" else torch.bfloat16
+    q, k, v = rand_qkv(gen, B, S, H, tdt)
+    n = (S + 63) // 64
+    rp = np.arange(H * n + 1) * n
+    ci = np.tile(np.arange(n), H * n)
+    full = ops.BlockMask.from_host(rp, ci, 1, H, n)
+    if dtype == "fp8":
+        cs = [ops.quantize_fp8_blockwise(x.cuda()) for x in (q, k, v)]
+        args, kw = [c for c, _ in cs], {"scales": tuple(s_ for _, s_ in cs)}
+        ins = [of.dequantize_blockwise(c.cpu().numpy(), s_.cpu().numpy()) for c, s_ in cs]
+        tol = TOL8
+    else:
+        args, kw = [x.cuda() for x in (q, k, v)], {}
+        ins = [np64(x) for x in (q, k, v)]
+        tol = TOL16
+    dense = ops.block_sparse_attn_fwd(*args, None, key_scale=key_scale, **kw)
+    listed = ops.block_sparse_attn_fwd(*args, full, key_scale=key_scale, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(dense.view(torch.int16), listed.view(torch.int16))
+    kk = ins[1] if key_scale is None else og.enhance_first_frame_keys(ins[1], *key_scale)
+    O, _ = oa.attention(ins[0], kk, ins[2], rp, ci, 1.0 / math.sqrt(128), 1)
+    assert within_rounding(np64(dense), O, tdt, atol=tol), float(np.max(np.abs(np64(dense) - O)))
 
 
 def test_attention_strided_views_and_determinism():
