@@ -218,16 +218,18 @@ def test_checker_and_plan_kv128():
     assert order == [u for x in range(8) for u in range(U) if xcd[u] == x]
 
 
-@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
-def test_block_mass_selection_coverage_kv128(dtype):
+@pytest.mark.parametrize("dtype,key_scale", [(torch.bfloat16, None), (torch.float16, None),
+                                             (torch.bfloat16, (450, 1.4))])
+def test_block_mass_selection_coverage_kv128(dtype, key_scale):
     B, S, H = 1, 1090, 2
     q, k = positional(B, S, H, dtype, 41)
     sm = 1.0 / math.sqrt(128)
     qd, kd = q.cuda(), k.cuda()
-    _, lse = ops.block_sparse_attn_fwd(qd, kd, kd, None, sm_scale=sm, return_lse=True)
-    Md = ops.attn_block_mass(qd, kd, lse, sm_scale=sm, kv_block=128)
+    _, lse = ops.block_sparse_attn_fwd(qd, kd, kd, None, sm_scale=sm, return_lse=True, key_scale=key_scale)
+    Md = ops.attn_block_mass(qd, kd, lse, sm_scale=sm, kv_block=128, key_scale=key_scale)
     M = Md.cpu().numpy().astype(np.float64)
-    ref = ms.block_mass_all(np64(q), np64(k), sm, kv_block=128)
+    kref = np64(k) if key_scale is None else og.enhance_first_frame_keys(np64(k), *key_scale)
+    ref = ms.block_mass_all(np64(q), kref, sm, kv_block=128)
     assert M.shape == ref.shape
     assert np.all(np.abs(M - ref) <= MASS_ATOL + MASS_RTOL * ref), float(np.max(np.abs(M - ref)))
     m = ops.select_block_mask(Md, S, 0.8, 0.1, kv_block=128)
