@@ -63,7 +63,10 @@ __device__ inline int work_item(const int32_t* order, int chunk, int W, int np) 
 // at `lds`, a wave-uniform LDS byte address): inline asm so that the compiler
 // does not drain every pending load before each LDS read (it cannot tell
 // which tile a direct load writes); kernels wait on the vector-memory
-// counter themselves.
+// counter themselves.  The asm writes m0, which the compiler reports it
+// cannot treat as clobbered (a reserved register); the kernels that use it
+// emit no m0 access of their own (the generated code reads and writes m0
+// only in these statements), so nothing the compiler keeps there is lost.
 __device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
                : "memory", "m0");
