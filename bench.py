@@ -79,6 +79,30 @@ def traffic_from_profile(kernel_file: str, workload: str, src_hash: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def torch_sdpa_dense(qkv16, reps: int, event_ms):
+    """torch.nn.functional.scaled_dot_product_attention on the dense problem
+    (all keys), restricted to its fused flash / memory-efficient kernels: a
+    reference figure for the dense path, nothing of it enters the step.
+    ``qkv16``: 16-bit Q, K, V in BSHD; ``event_ms(fn, reps)`` times a launch.
+    Returns (ms, backend) or (None, None)."""
+    import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    q, k, v = (x.transpose(1, 2).contiguous() for x in qkv16)
+    try:
+        for name, be in (("flash", SDPBackend.FLASH_ATTENTION), ("efficient", SDPBackend.EFFICIENT_ATTENTION)):
+            try:
+                with sdpa_kernel(be):
+                    torch.nn.functional.scaled_dot_product_attention(q, k, v)
+                    torch.cuda.synchronize()
+                    ms = event_ms(lambda: torch.nn.functional.scaled_dot_product_attention(q, k, v), reps)
+                return ms, name
+            except RuntimeError:
+                continue
+        return None, None
+    finally:
+        del q, k, v
+
+
 def cpu_baseline(wl, inp, budget_s: float, gpu=None):
     """Oracle (plain NumPy float64) on a bounded sample of the same workload:
     head by head of request 0, the oracle mask builder for the head (or the
@@ -454,6 +478,7 @@ def main():
     del vmap, refreshed, ws_visit
     dense_reps = max(3, reps // 4)
     dense_ms = event_ms(lambda: attn(mask, None, dense=True), dense_reps)
+    sdpa_ms, sdpa_backend = torch_sdpa_dense((q, k, v), dense_reps, event_ms)
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[wl.dtype]
 
@@ -504,6 +529,10 @@ def main():
         "visit_refresh_worst_ms": round(visit_refresh_ms, 4),
         "routing_overhead_ratio": round(build_ms / (build_ms + attn_ms), 4),
         "dense_attn_ms": round(dense_ms, 4),
+        # for scale: torch's own fused attention (flash / memory-efficient
+        # backends only) on the same dense problem in 16 bits
+        "torch_sdpa_dense_ms": None if sdpa_ms is None else round(sdpa_ms, 4),
+        "torch_sdpa_backend": sdpa_backend,
         "speedup_vs_dense": round(dense_ms / attn_ms, 3),
         "ideal_speedup": round(float(mask.rows * n) / sub, 3),
         "roofline": {
