@@ -516,6 +516,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const void* __restr
 // share a workgroup.
 // ---------------------------------------------------------------------------
 constexpr int kWaveMaxPer = 32;   // n <= 2048
+constexpr int kTopScan = 3;       // distinct first-digit values walked before the histogram
 
 // LDS accesses of one wave take effect in program order; this keeps the
 // compiler from moving them across the point.
@@ -605,7 +606,55 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
     uint64_t prefix = lo == 64 ? 0 : (kmin >> lo) << lo;
     uint64_t mass_above = 0;
     uint32_t cnt_above = 0, bin_cnt = (uint32_t)n;
-    while (lo > 0) {
+    // The first digit (below the bits all keys share) takes few values across
+    // a row (the sign and top exponent bits of the scores), so histogram adds
+    // would pile onto a handful of LDS words.  Walk its distinct values from
+    // the top with wave reductions instead; after kTopScan values without the
+    // boundary, the histogram takes the remaining (smaller) digits.
+    int dig_limit = 256;
+    if (lo > 0) {
+      const int shift = lo > 8 ? lo - 8 : 0;
+      for (int it = 0; it < kTopScan; ++it) {
+        int dmax = -1;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+          const int j = lane + 64 * e;
+          const int d = (int)((key[e] >> shift) & 255);
+          if (j < n && (lo == 64 || ((key[e] ^ prefix) >> lo) == 0) && d < dig_limit) dmax = d > dmax ? d : dmax;
+        }
+        for (int o = 32; o > 0; o >>= 1) {
+          const int w = __shfl_xor(dmax, o);
+          dmax = w > dmax ? w : dmax;
+        }
+        if (dmax < 0) break;
+        uint32_t c = 0;
+        uint64_t m = 0;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) {
+          const int j = lane + 64 * e;
+          if (j < n && (lo == 64 || ((key[e] ^ prefix) >> lo) == 0) && (int)((key[e] >> shift) & 255) == dmax) {
+            ++c;
+            m += mass[e];
+          }
+        }
+        for (int o = 32; o > 0; o >>= 1) {
+          c += __shfl_xor(c, o);
+          m += __shfl_xor(m, o);
+        }
+        if (cond(cnt_above + c, mass_above + m)) {
+          // the boundary block has this digit
+          prefix = (prefix & ~(255ull << shift)) | ((uint64_t)dmax << shift);
+          lo = shift;
+          bin_cnt = c;
+          dig_limit = 256;
+          break;
+        }
+        cnt_above += c;
+        mass_above += m;
+        dig_limit = dmax;
+      }
+    }
+    while (lo > 0 && bin_cnt > 1) {
       const int shift = lo > 8 ? lo - 8 : 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -616,7 +665,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
 #pragma unroll
       for (int e = 0; e < PER; ++e) {
         const int j = lane + 64 * e;
-        if (j < n && (lo == 64 || ((key[e] ^ prefix) >> lo) == 0)) {
+        if (j < n && (lo == 64 || ((key[e] ^ prefix) >> lo) == 0) && (int)((key[e] >> shift) & 255) < dig_limit) {
           const int bin = (int)((key[e] >> shift) & 255);
           atomicAdd(&hist_cnt[bin], 1u);
           atomicAdd((unsigned long long*)&hist_mass[bin], (unsigned long long)mass[e]);
@@ -671,6 +720,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
       bin_cnt = wave_bcast(f_bin_cnt, src);
       prefix = (prefix & ~(255ull << shift)) | ((uint64_t)bin << shift);
       lo = shift;
+      dig_limit = 256;
       if (bin_cnt == 1) break;
     }
     if (bin_cnt == 1) {
