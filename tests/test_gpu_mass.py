@@ -12,7 +12,7 @@ from oracle import mask as om
 from oracle import mass as ms
 from paper_2606_25040_amd import ops
 from paper_2606_25040_amd import workloads as wk
-from tests.compare import compare_masks
+from tests.compare import compare_masks, compare_row
 
 pytestmark = pytest.mark.gpu
 
@@ -117,6 +117,37 @@ def test_selection_of_exact_mass_ties_and_zero_rows():
         if top_p > 0:
             r = (0 * H + 1) * n + 3
             assert list(ci[rp[r]:rp[r + 1]]) == list(range(n))
+
+
+@pytest.mark.parametrize("n", [300, 1182, 2048])
+@pytest.mark.parametrize("top_p,mk", [(0.5, 0.0), (0.999999, 0.0), (0.9999, 0.6), (0.3, 0.95)])
+def test_selection_over_masses_spanning_many_magnitudes(n, top_p, mk):
+    """Masses spread log-uniformly over 30 decades give the first radix digit
+    of the keys (sign and top exponent bits) several distinct values, and
+    top_p near 1 or a large floor puts the boundary deep in the order: the
+    selection's walk over the first digit's top values runs out and the
+    histogram takes over.  Same masses on both sides: exact agreement."""
+    H = 2
+    S = 64 * n
+    rng = np.random.Generator(np.random.PCG64(n))
+    M = (10.0 ** rng.uniform(-30, 0, (1, H, 8, n))).astype(np.float32)
+    M[0, 1, 5, rng.integers(0, n, n // 3)] = 0.0             # zero-mass blocks in one row
+    # a q-block count of 8 rows per head: pad the mass tensor to the n q-blocks S implies
+    Mfull = np.zeros((1, H, n, n), np.float32)
+    Mfull[:, :, :8] = M
+    Mfull[:, :, 8:] = 1.0 / n
+    Md = torch.from_numpy(Mfull).cuda()
+    m = ops.select_block_mask(Md, S, top_p, mk)
+    rp, ci = m.to_host()
+    assert ops.validate_block_mask(m) == 0
+    for h in range(H):
+        for i in range(8):
+            r = h * n + i
+            row = Mfull[0, h, i].astype(np.float64)
+            with np.errstate(divide="ignore"):
+                res = compare_row(ci[rp[r]:rp[r + 1]], ms.select_row_from_mass(row, top_p, mk), np.log(row),
+                                  top_p, mk)
+            assert res in ("exact", "excused"), (h, i, res)
 
 
 def test_coverage_matches_oracle():
