@@ -213,6 +213,7 @@ __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ q
 // selection is deterministic.
 // ---------------------------------------------------------------------------
 constexpr int kSelThreads = 256;
+constexpr int kTopScan = 3;   // distinct first-digit values walked before the histogram
 constexpr double kMassOne = 4611686018427387904.0;          // 2^62
 static_assert(kSelThreads == 256, "one histogram bin per thread");
 
@@ -376,14 +377,51 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const void* __restr
     uint64_t prefix = lo == 64 ? 0 : (kmin >> lo) << lo;
     uint64_t mass_above = 0;
     uint32_t cnt_above = 0, bin_cnt = (uint32_t)n;
-    while (lo > 0) {
+    // first digit: its few distinct values walked from the top with block
+    // reductions (as in the wave kernel below), the histogram after that
+    int dig_limit = 256;
+    if (lo > 0) {
+      const int shift = lo > 8 ? lo - 8 : 0;
+      for (int it = 0; it < kTopScan; ++it) {
+        uint64_t dm = 0;   // 1 + the largest digit below dig_limit, 0 if none
+        for (int j = tid; j < n; j += kSelThreads) {
+          const uint64_t kj = key[j];
+          const uint64_t d = (kj >> shift) & 255;
+          if ((lo == 64 || ((kj ^ prefix) >> lo) == 0) && (int)d < dig_limit && d + 1 > dm) dm = d + 1;
+        }
+        dm = block_reduce_max_u64(dm, red64);
+        if (dm == 0) break;
+        const uint64_t dmax = dm - 1;
+        uint64_t c = 0, m = 0;
+        for (int j = tid; j < n; j += kSelThreads) {
+          const uint64_t kj = key[j];
+          if ((lo == 64 || ((kj ^ prefix) >> lo) == 0) && ((kj >> shift) & 255) == dmax) {
+            ++c;
+            m += mass[j];
+          }
+        }
+        c = block_reduce_sum_u64(c, red64);
+        m = block_reduce_sum_u64(m, red64);
+        if (cond(cnt_above + (uint32_t)c, mass_above + m)) {
+          prefix = (prefix & ~(255ull << shift)) | (dmax << shift);
+          lo = shift;
+          bin_cnt = (uint32_t)c;
+          dig_limit = 256;
+          break;
+        }
+        cnt_above += (uint32_t)c;
+        mass_above += m;
+        dig_limit = (int)dmax;
+      }
+    }
+    while (lo > 0 && bin_cnt > 1) {
       const int shift = lo > 8 ? lo - 8 : 0;
       hist_cnt[tid] = 0u;
       hist_mass[tid] = 0ull;
       __syncthreads();
       for (int j = tid; j < n; j += kSelThreads) {
         const uint64_t kj = key[j];
-        if (lo == 64 || ((kj ^ prefix) >> lo) == 0) {
+        if ((lo == 64 || ((kj ^ prefix) >> lo) == 0) && (int)((kj >> shift) & 255) < dig_limit) {
           const int bin = (int)((kj >> shift) & 255);
           atomicAdd(&hist_cnt[bin], 1u);
           atomicAdd((unsigned long long*)&hist_mass[bin], (unsigned long long)mass[j]);
@@ -436,6 +474,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const void* __restr
       mass_above = sel_mass_above;
       bin_cnt = sel_bin_cnt;
       lo = shift;
+      dig_limit = 256;
       if (bin_cnt == 1) break;
     }
     if (bin_cnt == 1) {
@@ -516,7 +555,6 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const void* __restr
 // share a workgroup.
 // ---------------------------------------------------------------------------
 constexpr int kWaveMaxPer = 32;   // n <= 2048
-constexpr int kTopScan = 3;       // distinct first-digit values walked before the histogram
 
 // LDS accesses of one wave take effect in program order; this keeps the
 // compiler from moving them across the point.

@@ -119,7 +119,7 @@ def test_selection_of_exact_mass_ties_and_zero_rows():
             assert list(ci[rp[r]:rp[r + 1]]) == list(range(n))
 
 
-@pytest.mark.parametrize("n", [300, 1182, 2048])
+@pytest.mark.parametrize("n", [300, 1182, 2048, 3000, 4096])
 @pytest.mark.parametrize("top_p,mk", [(0.5, 0.0), (0.999999, 0.0), (0.9999, 0.6), (0.3, 0.95)])
 def test_selection_over_masses_spanning_many_magnitudes(n, top_p, mk):
     """Masses spread log-uniformly over 30 decades give the first radix digit
