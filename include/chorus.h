@@ -231,6 +231,8 @@ chorus_status chorus_validate_block_mask(const chorus_block_mask* mask, int64_t 
  * (b, h, 64-token block) over its valid tokens x 128 values:
  *   amax = max|x|; inv = fp32(448 / amax); code = e4m3fn_rne(clamp(x * inv,
  *   -448, 448)); scale = fp32(amax / 448); amax == 0 gives codes +-0, scale 1.
+ *   A block with amax < 2^-64 takes x and amax times 2^64 (exact) before the
+ *   reciprocal, so that it stays finite; the codes depend on x / amax only.
  * x      : [B, S, H, D] f16 or bf16 (in_dtype).
  * codes  : out [B, S, H, D] uint8 (its own strides, in bytes == elements).
  * scales : out device float32 [B, H, n_blocks], contiguous.
