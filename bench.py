@@ -9,6 +9,10 @@ workload], and the block-sparse attention forward pass.  The metric is the
 effective TFLOP/s on computed blocks, 4 * 64 * 64 * 128 FLOP per computed
 (q-block, kv-block) pair, over the measured time.  Prints ONE JSON line.
 
+The default workload is the largest one that fits one GPU: four similar
+requests (B 4, H 40, S 32,760 on a 21 x 30 x 52 latent grid, bf16) sharing one
+15 %-density mask built from request 0.
+
 Beside the step throughput the line carries: the attention kernel's own
 throughput and MFMA-roofline fraction (HIP events on the launch stream), the
 builder time and the routing-overhead ratio routing / (routing + attention)
@@ -34,7 +38,7 @@ if ROOT not in sys.path:
 
 PEAK_TFLOPS = {"bf16": 2516.6, "f16": 2516.6, "fp8": 5033.2}   # 256 CU x 2.4 GHz x 4096 / 8192
 FLOP_PER_PAIR = 4 * 64 * 64 * 128
-DEFAULT_WORKLOAD = "wan5b_720p_bf16"
+DEFAULT_WORKLOAD = "wan14b_480p_batch4_bf16"
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -77,30 +81,6 @@ def traffic_from_profile(kernel_file: str, workload: str, src_hash: str):
     if rec.get("source_hash") != src_hash or rec.get("kernel_file") != kernel_file:
         return None
     return rec.get("hbm_bytes_per_launch")
-
-
-def torch_sdpa_dense(qkv16, reps: int, event_ms):
-    """torch.nn.functional.scaled_dot_product_attention on the dense problem
-    (all keys), restricted to its fused flash / memory-efficient kernels: a
-    reference figure for the dense path, nothing of it enters the step.
-    ``qkv16``: 16-bit Q, K, V in BSHD; ``event_ms(fn, reps)`` times a launch.
-    Returns (ms, backend) or (None, None)."""
-    import torch
-    from torch.nn.attention import SDPBackend, sdpa_kernel
-    q, k, v = (x.transpose(1, 2).contiguous() for x in qkv16)
-    try:
-        for name, be in (("flash", SDPBackend.FLASH_ATTENTION), ("efficient", SDPBackend.EFFICIENT_ATTENTION)):
-            try:
-                with sdpa_kernel(be):
-                    torch.nn.functional.scaled_dot_product_attention(q, k, v)
-                    torch.cuda.synchronize()
-                    ms = event_ms(lambda: torch.nn.functional.scaled_dot_product_attention(q, k, v), reps)
-                return ms, name
-            except RuntimeError:
-                continue
-        return None, None
-    finally:
-        del q, k, v
 
 
 def cpu_baseline(wl, inp, budget_s: float, gpu=None):
@@ -200,7 +180,7 @@ def coverage_study(args) -> None:
     import torch
 
     from paper_2606_25040_amd import ops
-    from paper_2606_25040_amd import workloads as wk
+    import workloads as wk
 
     torch.cuda.set_device(0)
     ops.load_library()
@@ -293,7 +273,7 @@ def main():
     import torch
 
     from paper_2606_25040_amd import ops
-    from paper_2606_25040_amd import workloads as wk
+    import workloads as wk
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
@@ -478,7 +458,6 @@ def main():
     del vmap, refreshed, ws_visit
     dense_reps = max(3, reps // 4)
     dense_ms = event_ms(lambda: attn(mask, None, dense=True), dense_reps)
-    sdpa_ms, sdpa_backend = torch_sdpa_dense((q, k, v), dense_reps, event_ms)
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[wl.dtype]
 
@@ -529,10 +508,6 @@ def main():
         "visit_refresh_worst_ms": round(visit_refresh_ms, 4),
         "routing_overhead_ratio": round(build_ms / (build_ms + attn_ms), 4),
         "dense_attn_ms": round(dense_ms, 4),
-        # for scale: torch's own fused attention (flash / memory-efficient
-        # backends only) on the same dense problem in 16 bits
-        "torch_sdpa_dense_ms": None if sdpa_ms is None else round(sdpa_ms, 4),
-        "torch_sdpa_backend": sdpa_backend,
         "speedup_vs_dense": round(dense_ms / attn_ms, 3),
         "ideal_speedup": round(float(mask.rows * n) / sub, 3),
         "roofline": {

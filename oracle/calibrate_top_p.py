@@ -8,7 +8,7 @@ mean density over all rows is X within 0.25 percentage points, then moved to
 the middle of the widest nearby gap between any row's cumulative masses, so
 that no row sits within rounding of its top-p boundary.
 
-Prints the values to freeze in ``paper_2606_25040_amd/workloads.py``.
+Prints the values to freeze in ``workloads.py``.
 Test infrastructure: calls only ``oracle/`` and the input generator.
 
     python -m oracle.calibrate_top_p [workload ...]
@@ -22,7 +22,7 @@ import time
 import numpy as np
 
 from oracle import mask as om
-from paper_2606_25040_amd import workloads as wk
+import workloads as wk
 
 
 def cumulative_rows(q, k, sm_scale):

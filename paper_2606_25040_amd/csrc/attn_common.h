@@ -42,34 +42,48 @@ __device__ inline float pair_sum(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Work item of dispatch slot p.  Items are runs of neighbouring q-blocks
-// (one q-block, or a pair), `np` per (request, head) unit, numbered
-// unit * np + index.  Slots are dealt
-// round-robin to the 8 XCDs, so slot p runs on XCD p % 8; XCD x walks item
-// positions [x * chunk, (x + 1) * chunk) of the unit order (the planned
-// order of (request, head) units, or the natural one).  Returns -1 for idle
-// slots.
-__device__ inline int work_item(const int32_t* order, int chunk, int W, int np) {
+// Work item of dispatch slot p.  Items are runs of neighbouring q-blocks,
+// `np` per (request, head) unit, numbered unit * np + index.  Slots are dealt
+// round-robin to the 8 XCDs, so slot p runs on XCD x = p % 8 as its
+// (p / 8)-th slot there.  XCD x owns the units at positions
+// [start(x), start(x) + cap(x)) of the unit order (the planned order of
+// (request, head) units, or the natural one), cap(x) = U / 8 plus one for
+// the first U % 8 XCDs -- the split the plan balances -- and walks their
+// items in order.  The grid holds ceil(U / 8) * np slots per XCD; slots past
+// an XCD's share return -1.
+__device__ inline int work_item(const int32_t* order, int U, int np) {
   const int p = blockIdx.x;
-  const int pos = (p % kNumXcd) * chunk + p / kNumXcd;
-  if (pos >= W) return -1;
-  if (!order) return pos;
-  const int unit = order[pos / np];
-  const int item = unit * np + pos % np;
-  return (unit >= 0 && item < W) ? item : -1;
+  const int x = p % kNumXcd, k = p / kNumXcd;
+  const int base = U / kNumXcd, extra = U % kNumXcd;
+  const int cap = base + (x < extra ? 1 : 0);
+  if (k >= cap * np) return -1;
+  const int pos = x * base + min(x, extra) + k / np;
+  const int unit = order ? order[pos] : pos;
+  return (unit >= 0 && unit < U) ? unit * np + k % np : -1;
 }
+inline unsigned work_grid(int U, int np) { return (unsigned)(kNumXcd * ((U + kNumXcd - 1) / kNumXcd) * np); }
 
 // One global -> LDS direct load (16 bytes per lane, lane-linear destination
-// at `lds`, a wave-uniform LDS byte address): inline asm so that the compiler
-// does not drain every pending load before each LDS read (it cannot tell
-// which tile a direct load writes); kernels wait on the vector-memory
-// counter themselves.  The asm writes m0, which the compiler reports it
-// cannot treat as clobbered (a reserved register); the kernels that use it
-// emit no m0 access of their own (the generated code reads and writes m0
-// only in these statements), so nothing the compiler keeps there is lost.
+// at `lds`, a wave-uniform LDS byte address).  The LDS address travels in
+// m0; the statement saves m0 to a scratch SGPR, sets it, waits the one wait
+// state an m0 write needs before an LDS-DMA read of it, issues the load and
+// puts m0 back, so whatever the compiler keeps in m0 is unchanged after it.
+// Inline asm rather than __builtin_amdgcn_global_load_lds: the compiler
+// cannot tell which tile a direct load writes, and with the builtin it waits
+// for every outstanding load (vmcnt(0)) before the next LDS read of any tile,
+// which drains the prefetch of the following tile; the kernels wait on the
+// vector-memory counter themselves.
 __device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
-               : "memory", "m0");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds), "v"(voff), "s"(sbase)
+      : "memory");
 }
 
 // Wait until at most n vector-memory loads of this wave are outstanding.

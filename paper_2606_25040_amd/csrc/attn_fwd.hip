@@ -116,14 +116,14 @@ struct TileLoader {
 
 template <bool BF16, bool DENSE, bool KSCALE, bool KV2>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
-void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
+void attn_fwd_16_kernel(AttnArgs a) {
   using E = Elt<BF16>;
   using vec8 = typename E::vec8;
   using scalar = typename E::scalar;
   __shared__ __attribute__((aligned(1024))) char k_s[kTileBytes];
   __shared__ __attribute__((aligned(1024))) char v_s[kTileBytes];
 
-  const int item = work_item(a.order, chunk, W, a.n);
+  const int item = work_item(a.order, a.B * a.H, a.n);
   if (item < 0) return;
   const int n = a.n, H = a.H, S = a.S;
   const int i = item % n;
@@ -338,32 +338,30 @@ void attn_fwd_16_kernel(AttnArgs a, int chunk, int W) {
 
 namespace {
 template <bool BF16, bool DENSE, bool KV2>
-void launch_16(const AttnArgs& a, dim3 grid, int chunk, int W, hipStream_t st) {
+void launch_16(const AttnArgs& a, dim3 grid, hipStream_t st) {
   if (a.ks.n_first > 0)
-    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, true, KV2>), grid, dim3(128), 0, st, a, chunk, W);
+    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, true, KV2>), grid, dim3(128), 0, st, a);
   else
-    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, false, KV2>), grid, dim3(128), 0, st, a, chunk, W);
+    hipLaunchKernelGGL((attn_fwd_16_kernel<BF16, DENSE, false, KV2>), grid, dim3(128), 0, st, a);
 }
 
 template <bool BF16>
-void launch_16_mask(const AttnArgs& a, dim3 grid, int chunk, int W, hipStream_t st) {
+void launch_16_mask(const AttnArgs& a, dim3 grid, hipStream_t st) {
   if (a.row_ptr == nullptr)
-    launch_16<BF16, true, false>(a, grid, chunk, W, st);
+    launch_16<BF16, true, false>(a, grid, st);
   else if (a.kv_block == 2 * kBlock)
-    launch_16<BF16, false, true>(a, grid, chunk, W, st);
+    launch_16<BF16, false, true>(a, grid, st);
   else
-    launch_16<BF16, false, false>(a, grid, chunk, W, st);
+    launch_16<BF16, false, false>(a, grid, st);
 }
 }  // namespace
 
 hipError_t launch_attn_fwd_16(chorus_dtype dt, const AttnArgs& a, hipStream_t st) {
-  const int W = a.B * a.H * a.n;
-  const int chunk = (W + kNumXcd - 1) / kNumXcd;
-  const dim3 grid(chunk * kNumXcd);
+  const dim3 grid(work_grid(a.B * a.H, a.n));
   if (dt == CHORUS_BF16)
-    launch_16_mask<true>(a, grid, chunk, W, st);
+    launch_16_mask<true>(a, grid, st);
   else
-    launch_16_mask<false>(a, grid, chunk, W, st);
+    launch_16_mask<false>(a, grid, st);
   return hipGetLastError();
 }
 

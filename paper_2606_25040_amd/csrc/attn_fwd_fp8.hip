@@ -87,11 +87,11 @@ struct Tile8Loader {
 
 template <bool DENSE, bool KSCALE, bool KV2>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
-void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
+void attn_fwd_fp8_kernel(AttnArgs a, int np) {
   __shared__ __attribute__((aligned(1024))) uint8_t tiles[2][2][kTile8];   // [buffer][K, V]
   __shared__ float red[kWaves];
 
-  const int item = work_item(a.order, chunk, W, np);
+  const int item = work_item(a.order, a.B * a.H, np);
   if (item < 0) return;
   const int n = a.n, H = a.H, S = a.S;
   const int ip = item % np;
@@ -311,25 +311,23 @@ void attn_fwd_fp8_kernel(AttnArgs a, int chunk, int W, int np) {
 
 hipError_t launch_attn_fwd_fp8(const AttnArgs& a, hipStream_t st) {
   const int np = (a.n + 1) / 2;
-  const int W = a.B * a.H * np;
-  const int chunk = (W + kNumXcd - 1) / kNumXcd;
-  const dim3 grid(chunk * kNumXcd), block(64 * kWaves);
+  const dim3 grid(work_grid(a.B * a.H, np)), block(64 * kWaves);
   const bool ks = a.ks.n_first > 0;
   if (a.row_ptr == nullptr) {
     if (ks)
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, true, false>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, true, false>), grid, block, 0, st, a, np);
     else
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, false, false>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<true, false, false>), grid, block, 0, st, a, np);
   } else if (a.kv_block == 2 * kBlock) {
     if (ks)
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, true, true>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, true, true>), grid, block, 0, st, a, np);
     else
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, false, true>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, false, true>), grid, block, 0, st, a, np);
   } else {
     if (ks)
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, true, false>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, true, false>), grid, block, 0, st, a, np);
     else
-      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, false, false>), grid, block, 0, st, a, chunk, W, np);
+      hipLaunchKernelGGL((attn_fwd_fp8_kernel<false, false, false>), grid, block, 0, st, a, np);
   }
   return hipGetLastError();
 }

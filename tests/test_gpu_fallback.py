@@ -12,7 +12,7 @@ import torch
 from oracle import attention as oa
 from oracle import fallback as fb
 from paper_2606_25040_amd import ops
-from paper_2606_25040_amd import workloads as wk
+import workloads as wk
 
 pytestmark = pytest.mark.gpu
 

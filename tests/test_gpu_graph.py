@@ -8,7 +8,7 @@ import pytest
 import torch
 
 from paper_2606_25040_amd import ops
-from paper_2606_25040_amd import workloads as wk
+import workloads as wk
 
 pytestmark = pytest.mark.gpu
 

@@ -15,7 +15,7 @@ from oracle import guidance as og
 from oracle import mask as om
 from oracle import mass as ms
 from paper_2606_25040_amd import ops
-from paper_2606_25040_amd import workloads as wk
+import workloads as wk
 from tests.compare import compare_masks, max_abs_err
 
 pytestmark = pytest.mark.gpu

@@ -17,7 +17,7 @@ from oracle import fp8 as of
 from oracle import guidance as og
 from oracle import mask as om
 from paper_2606_25040_amd import ops
-from paper_2606_25040_amd import workloads as wk
+import workloads as wk
 from tests.compare import compare_masks, max_abs_err
 
 pytestmark = pytest.mark.gpu
@@ -469,53 +469,59 @@ def test_full_size_mask_sampled_heads(key):
     assert ops.validate_block_mask(mask) == 0
 
 
-def _sample_items(wl, rng, per_head=3):
+def _check_heads(wl, out, lse, rp, ci, ins, heads, tol):
+    """Every q-block (the partial last one included) of the listed heads of
+    every request against the oracle, outputs and LSE.  ``ins(b, h)`` gives
+    the float64 [S, D] q, k, v of (b, h) exactly as the kernel read them."""
     n = wl.n_blocks
-    items = []
+    worst = worst_lse = 0.0
     for b in range(wl.B):
-        for h in range(wl.H):
-            picks = {0, n - 1} | set(rng.integers(0, n, size=per_head).tolist())
-            items += [(b, h, i) for i in sorted(picks)]
-    return items
+        for h in heads:
+            qh, kh, vh = ins(b, h)
+            oh = np64(out[b, :, h].cpu())
+            lh = lse[b, h].cpu().numpy().astype(np.float64)
+            for i in range(n):
+                r = oa.mask_row_index(b, h, i, wl.H, n, 1)
+                o_ref, l_ref = oa.attention_block(qh, kh, vh, oa.row_blocks(rp, ci, r), i, wl.sm_scale)
+                rows = slice(i * 64, i * 64 + o_ref.shape[0])
+                worst = max(worst, max_abs_err(oh[rows], o_ref))
+                worst_lse = max(worst_lse, max_abs_err(lh[rows], l_ref))
+    assert worst <= tol, worst
+    assert worst_lse <= 1e-3, worst_lse
+    return worst
 
 
 @pytest.mark.parametrize("key", FULL)
-def test_full_size_attention_sampled(key):
+def test_full_size_attention_every_q_block_of_two_heads(key):
+    """Full-size launch (planned XCD order, as the benchmark runs it): every
+    q-block of the sharpest and the most diffuse head of every request
+    against the oracle; the unplanned order gives bitwise the same output."""
     st = workload_state(key)
     wl, mask = st["wl"], st["mask"]
     rp, ci = mask.to_host()
     order = ops.plan_block_mask(mask, wl.B, wl.S)
     if wl.dtype == "fp8":
         (qc, qs), (kc, ks), (vc, vs) = st["q8"], st["k8"], st["v8"]
-        out = ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs), schedule=order)
+        out, lse = ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs), schedule=order,
+                                             return_lse=True)
+        out2 = ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs))
         tol = TOL8
-    else:
-        out = ops.block_sparse_attn_fwd(st["q"], st["k"], st["v"], mask, schedule=order)
-        tol = TOL16
-    out2 = (ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs))
-            if wl.dtype == "fp8" else ops.block_sparse_attn_fwd(st["q"], st["k"], st["v"], mask))
-    torch.cuda.synchronize()
-    assert torch.equal(out.view(torch.int16), out2.view(torch.int16))
-    rng = np.random.Generator(np.random.PCG64(wl.seed))
-    items = _sample_items(wl, rng, per_head=2 if wl.B > 1 else 3)
-    n = wl.n_blocks
-    worst = 0.0
-    by_head = {}
-    for b, h, i in items:
-        by_head.setdefault((b, h), []).append(i)
-    for (b, h), blocks in by_head.items():
-        if wl.dtype == "fp8":
+
+        def ins(b, h):
             sl = lambda c, s: of.dequantize_blockwise(c[b:b + 1, :, h:h + 1].cpu().numpy(),
                                                       s[b:b + 1, h:h + 1].cpu().numpy())[0, :, 0]
-            qh, kh, vh = sl(qc, qs), sl(kc, ks), sl(vc, vs)
-        else:
-            qh, kh, vh = (np64(x[b, :, h].cpu()) for x in (st["q"], st["k"], st["v"]))
-        oh = np64(out[b, :, h].cpu())
-        for i in blocks:
-            r = oa.mask_row_index(b, h, i, wl.H, n, 1)
-            o_ref, _ = oa.attention_block(qh, kh, vh, oa.row_blocks(rp, ci, r), i, wl.sm_scale)
-            worst = max(worst, max_abs_err(oh[i * 64:i * 64 + o_ref.shape[0]], o_ref))
-    assert worst <= tol, worst
+            return sl(qc, qs), sl(kc, ks), sl(vc, vs)
+    else:
+        out, lse = ops.block_sparse_attn_fwd(st["q"], st["k"], st["v"], mask, schedule=order,
+                                             return_lse=True)
+        out2 = ops.block_sparse_attn_fwd(st["q"], st["k"], st["v"], mask)
+        tol = TOL16
+
+        def ins(b, h):
+            return tuple(np64(x[b, :, h].cpu()).astype(np.float64) for x in (st["q"], st["k"], st["v"]))
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), out2.view(torch.int16))
+    _check_heads(wl, out, lse, rp, ci, ins, (0, wl.H - 1), tol)
 
 
 def test_plan_beyond_4096_units_keeps_natural_order_and_results():
@@ -537,3 +543,58 @@ def test_plan_beyond_4096_units_keeps_natural_order_and_results():
     out = ops.block_sparse_attn_fwd(q, k, v, mask, schedule=perm)
     torch.cuda.synchronize()
     assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+
+
+def test_tiny_f16_workload_every_element():
+    """The tiny f16 check (B 1, H 2, S 4096 on a 4 x 32 x 32 grid, fixed
+    random 25 % mask with the diagonal kept) through the C ABI: every output
+    element and every LSE against the oracle's literal form (64 x S logits per
+    q-block, unlisted blocks at -inf), plain and planned launch order."""
+    wl = wk.WORKLOADS["tiny_f16"]
+    inp = wk.make_inputs(wl)
+    rp, ci = inp.random_mask
+    mask = ops.BlockMask.from_host(rp, ci, 1, wl.H, wl.n_blocks)
+    q, k, v = inp.q.cuda(), inp.k.cuda(), inp.v.cuda()
+    out, lse = ops.block_sparse_attn_fwd(q, k, v, mask, sm_scale=wl.sm_scale, return_lse=True)
+    order = ops.plan_block_mask(mask, wl.B, wl.S)
+    out2 = ops.block_sparse_attn_fwd(q, k, v, mask, sm_scale=wl.sm_scale, schedule=order)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), out2.view(torch.int16))
+    O, L = oa.attention(np64(inp.q), np64(inp.k), np64(inp.v), rp, ci, wl.sm_scale, 1, form="literal")
+    assert max_abs_err(np64(out), O) <= TOL16
+    assert max_abs_err(lse.cpu().numpy(), L) <= 1e-3
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("B,H", [(1, 13), (3, 3), (1, 1)])
+def test_planned_order_with_units_not_a_multiple_of_eight(dtype, B, H):
+    """B * H (request, head) units not a multiple of the 8 XCDs: each XCD
+    walks exactly the units the plan gave it; any order gives bitwise the
+    same output, and it matches the oracle."""
+    gen = torch.Generator().manual_seed(B * 100 + H)
+    S = 700
+    q, k, v = rand_qkv(gen, B, S, H, torch.bfloat16)
+    n = (S + 63) // 64
+    rng = np.random.Generator(np.random.PCG64(B * 7 + H))
+    rp, ci = wk.random_csr(rng, H * n, n, 0.4)
+    mask = ops.BlockMask.from_host(rp, ci, 1, H, n)
+    order = ops.plan_block_mask(mask, B, S)
+    assert sorted(order.cpu().tolist()) == list(range(B * H))
+    if dtype == "fp8":
+        cs = [ops.quantize_fp8_blockwise(x.cuda()) for x in (q, k, v)]
+        args, kw = [c for c, _ in cs], {"scales": tuple(s_ for _, s_ in cs)}
+        ins = [of.dequantize_blockwise(c.cpu().numpy(), s_.cpu().numpy()) for c, s_ in cs]
+        tol = TOL8
+    else:
+        args, kw = [x.cuda() for x in (q, k, v)], {}
+        ins = [np64(x) for x in (q, k, v)]
+        tol = TOL16
+    natural = ops.block_sparse_attn_fwd(*args, mask, **kw)
+    planned = ops.block_sparse_attn_fwd(*args, mask, schedule=order, **kw)
+    perm = torch.from_numpy(rng.permutation(B * H).astype(np.int32)).cuda()
+    shuffled = ops.block_sparse_attn_fwd(*args, mask, schedule=perm, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(natural.view(torch.int16), planned.view(torch.int16))
+    assert torch.equal(natural.view(torch.int16), shuffled.view(torch.int16))
+    O, _ = oa.attention(*ins, rp, ci, 1.0 / math.sqrt(128), 1)
+    assert within_rounding(np64(natural), O, torch.bfloat16, atol=tol)

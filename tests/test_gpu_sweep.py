@@ -14,7 +14,7 @@ from oracle import attention as oa
 from oracle import fp8 as of
 from oracle import mask as om
 from paper_2606_25040_amd import ops
-from paper_2606_25040_amd import workloads as wk
+import workloads as wk
 from tests.compare import compare_masks
 
 pytestmark = pytest.mark.gpu

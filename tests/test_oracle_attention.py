@@ -13,7 +13,7 @@ import torch
 from scipy.special import logsumexp
 
 from oracle import attention as oa
-from paper_2606_25040_amd.workloads import random_csr
+from workloads import random_csr
 
 
 def _rand_qkv(rng, B, S, H, D, scale=1.0):

@@ -13,7 +13,7 @@ from oracle import attention as oa
 from oracle import guidance as og
 from oracle import mask as om
 from oracle import mass as ms
-from paper_2606_25040_amd.workloads import random_csr
+from workloads import random_csr
 
 
 def test_first_frame_tokens():

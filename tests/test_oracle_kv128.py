@@ -12,7 +12,7 @@ import pytest
 from oracle import attention as oa
 from oracle import mask as om
 from oracle import mass as ms
-from paper_2606_25040_amd.workloads import random_csr
+from workloads import random_csr
 
 
 def expand(rp, ci, n64):

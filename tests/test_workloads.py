@@ -7,7 +7,7 @@ import torch
 
 from oracle import attention as oa
 from oracle import mask as om
-from paper_2606_25040_amd import workloads as wk
+import workloads as wk
 
 
 def small(key, **kw):
