@@ -55,6 +55,10 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay of the step")
     ap.add_argument("--f16", action="store_true",
                     help="run a 16-bit workload in f16 (its inputs converted) instead of bf16")
+    ap.add_argument("--head-schedule", action="store_true",
+                    help="instead of the throughput line, time the attention of the fp8 720p 14B workload on "
+                         "each of 8 five-head sets (the one-GPU share of an 8-GPU head-parallel layout): the "
+                         "plan's balanced sets against contiguous slices")
     ap.add_argument("--coverage", action="store_true",
                     help="instead of the throughput line, print the mask-coverage study (true block-mass "
                          "masks of a historical request reused on similar requests)")
@@ -261,6 +265,78 @@ def coverage_study(args) -> None:
     print(json.dumps(line), flush=True)
 
 
+def head_schedule_study(args) -> None:
+    """The one-GPU share of head-parallel attention (Sec. 3.2 "Head-level
+    scheduling for load balancing", Appendix A): the 40 heads of the 720p 14B
+    fp8 workload are split into 8 sets of 5, one per rank of an 8-GPU layout,
+    either as contiguous slices or as the plan's balanced sets (the plan deals
+    units heaviest first to the least-loaded of 8 bins of equal capacity --
+    the rule the paper applies to GPUs, here read off the plan's unit order,
+    5 units per bin).  Each set's attention (its heads' Q/K/V codes and mask
+    rows) is launched alone on this GPU and timed; the imbalance is the
+    max / mean of the 8 set times.  One JSON line."""
+    import torch
+
+    from paper_2606_25040_amd import ops
+    import workloads as wk
+
+    torch.cuda.set_device(0)
+    ops.load_library()
+    wl = wk.WORKLOADS["wan14b_720p_fp8"]
+    G = 8
+    inp = wk.make_inputs(wl)
+    H, n, S = wl.H, wl.n_blocks, wl.S
+    q, k, v = inp.q.cuda(), inp.k.cuda(), inp.v.cuda()
+    mask = ops.build_block_mask(inp.mask_q.cuda(), inp.mask_k.cuda(), wl.top_p, wl.min_top_k,
+                                sm_scale=wl.sm_scale)
+    codes = [ops.quantize_fp8_blockwise(x) for x in (q, k, v)]
+    del q, k, v
+    order = ops.plan_block_mask(mask, 1, S).cpu().tolist()
+    rp, ci = mask.to_host()
+    cost = [int(rp[(h + 1) * n] - rp[h * n]) for h in range(H)]
+    per = H // G
+    sets = {"contiguous": [list(range(r * per, (r + 1) * per)) for r in range(G)],
+            "planned": [order[r * per:(r + 1) * per] for r in range(G)]}
+
+    def set_ms(heads):
+        idx = torch.tensor(heads, device="cuda")
+        cs = [(c.index_select(2, idx).contiguous(), s_.index_select(1, idx).contiguous()) for c, s_ in codes]
+        rows = [np.asarray(ci[rp[h * n + i]:rp[h * n + i + 1]]) for h in heads for i in range(n)]
+        sub_rp = np.zeros(len(rows) + 1, dtype=np.int64)
+        np.cumsum([len(r) for r in rows], out=sub_rp[1:])
+        sub = ops.BlockMask.from_host(sub_rp, np.concatenate(rows), 1, len(heads), n)
+        sched = ops.plan_block_mask(sub, 1, S)
+        out = torch.empty((1, S, len(heads), 128), dtype=torch.bfloat16, device="cuda")
+        fn = lambda: ops.block_sparse_attn_fwd(cs[0][0], cs[1][0], cs[2][0], sub, sm_scale=wl.sm_scale,
+                                               scales=(cs[0][1], cs[1][1], cs[2][1]), out=out, schedule=sched)
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        reps = 10
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        e1.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    result = {}
+    for name, ss in sets.items():
+        ms = [set_ms(hs) for hs in ss]
+        loads = [sum(cost[h] for h in hs) for hs in ss]
+        result[name] = {"heads": ss, "set_ms": [round(x, 4) for x in ms],
+                        "imbalance_time": round(max(ms) / (sum(ms) / G), 4),
+                        "listed_blocks": loads,
+                        "imbalance_listed_blocks": round(max(loads) / (sum(loads) / G), 4)}
+    line = {"study": "one-GPU share of head-level scheduling over 8 head sets (Sec. 3.2, Appendix A)",
+            "workload": wl.key, "sets": G, "heads_per_set": per, "dtype": "fp8",
+            "data": "synthetic (seeded Wan-class Q/K/V on the latent grid; no real latents)",
+            "paper_imbalance": {"without_scheduler": 1.34, "with_scheduler": 1.12},
+            "results": result}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -269,6 +345,9 @@ def main():
         sys.exit(2)
     if args.coverage:
         coverage_study(args)
+        return
+    if args.head_schedule:
+        head_schedule_study(args)
         return
     import torch
 

@@ -43,25 +43,27 @@ __device__ inline float pair_sum(float v) {
 }
 
 // Work item of dispatch slot p.  Items are runs of neighbouring q-blocks,
-// `np` per (request, head) unit, numbered unit * np + index.  Slots are dealt
-// round-robin to the 8 XCDs, so slot p runs on XCD x = p % 8 as its
-// (p / 8)-th slot there.  XCD x owns the units at positions
-// [start(x), start(x) + cap(x)) of the unit order (the planned order of
-// (request, head) units, or the natural one), cap(x) = U / 8 plus one for
-// the first U % 8 XCDs -- the split the plan balances -- and walks their
-// items in order.  The grid holds ceil(U / 8) * np slots per XCD; slots past
-// an XCD's share return -1.
+// `np` per (request, head) unit, numbered unit * np + index, listed in the
+// unit order (the planned order of (request, head) units, or the natural
+// one).  Slots are dealt round-robin to the 8 XCDs, so slot p runs on XCD
+// x = p % 8 as its (p / 8)-th slot there; XCD x walks item positions
+// [x * chunk, (x + 1) * chunk), chunk = ceil(U * np / 8), so all eight XCDs
+// share the work even when there are fewer than eight units.  When U is a
+// multiple of 8 each XCD's positions are exactly U / 8 whole units, the
+// runs the plan balances.  Returns -1 for idle slots.
 __device__ inline int work_item(const int32_t* order, int U, int np) {
   const int p = blockIdx.x;
+  const int W = U * np;
+  const int chunk = (W + kNumXcd - 1) / kNumXcd;
   const int x = p % kNumXcd, k = p / kNumXcd;
-  const int base = U / kNumXcd, extra = U % kNumXcd;
-  const int cap = base + (x < extra ? 1 : 0);
-  if (k >= cap * np) return -1;
-  const int pos = x * base + min(x, extra) + k / np;
-  const int unit = order ? order[pos] : pos;
-  return (unit >= 0 && unit < U) ? unit * np + k % np : -1;
+  const int pos = x * chunk + k;
+  if (k >= chunk || pos >= W) return -1;
+  const int unit = order ? order[pos / np] : pos / np;
+  return (unit >= 0 && unit < U) ? unit * np + pos % np : -1;
 }
-inline unsigned work_grid(int U, int np) { return (unsigned)(kNumXcd * ((U + kNumXcd - 1) / kNumXcd) * np); }
+inline unsigned work_grid(int U, int np) {
+  return (unsigned)(kNumXcd * ((U * np + kNumXcd - 1) / kNumXcd));
+}
 
 // One global -> LDS direct load (16 bytes per lane, lane-linear destination
 // at `lds`, a wave-uniform LDS byte address).  The LDS address travels in
