@@ -189,6 +189,29 @@ chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const choru
                                           float* block_scores, void* workspace,
                                           size_t workspace_bytes, void* stream);
 
+/* The builder for callers that cannot allocate device memory (code under
+ * HIP-graph capture, serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, checks and result as chorus_build_block_mask on f16 / bf16
+ * input -- bitwise the same row_ptr, col_idx and block_scores -- without a
+ * workspace.  Its scratch is a fixed 64 MiB device array inside this library
+ * (one copy per GPU it runs on, held until the process ends); the first call
+ * on a device looks up that array's address, later calls allocate nothing
+ * and call no allocating routine.  The heads of each request are processed
+ * in chunks that fit the array, so a shape fits when the per-row counts and
+ * selection bitmaps of all B * H * n_blocks rows plus one head's float64
+ * pooled means and scores (2 * n_blocks * 128 + n_blocks * n_kv doubles) fit
+ * in 64 MiB; larger shapes return CHORUS_ERR_CAPACITY before anything is
+ * enqueued.  Every call on a GPU uses that GPU's one array: calls that
+ * overlap on one GPU (different streams, or host threads without ordering)
+ * race and must not be issued; calls ordered on one stream are safe.
+ * dtype CHORUS_FP8_E4M3 returns CHORUS_ERR_UNSUPPORTED. */
+chorus_status chorus_build_block_mask_noalloc(chorus_dtype dtype, const chorus_shape* shape,
+                                              const chorus_tensor* q, const chorus_tensor* k,
+                                              double sm_scale, double top_p, double min_top_k,
+                                              int32_t kv_block, const chorus_key_scale* key_scale,
+                                              int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                              float* block_scores, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Work plan -- the one-GPU counterpart of the paper's head-level scheduling
  * (Sec. 3.2 "Head-level scheduling for load balancing", Appendix A): because

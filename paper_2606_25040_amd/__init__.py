@@ -15,6 +15,7 @@ from .ops import (  # noqa: F401
     block_sparse_attn_fwd_f16,
     block_sparse_attn_fwd_fp8,
     build_block_mask,
+    build_block_mask_noalloc,
     load_library,
     mask_coverage,
     plan_block_mask,

@@ -154,13 +154,13 @@ size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape) {
   return bytes;
 }
 
-static chorus_status build_mask_impl(chorus_dtype dtype, const chorus_shape* shape, const chorus_tensor* q,
-                                     const float* q_scale, const chorus_tensor* k, const float* k_scale,
-                                     double sm_scale, double top_p, double min_top_k, int32_t kv_block,
-                                     const chorus_key_scale* key_scale, int32_t* row_ptr, int32_t* col_idx,
-                                     int64_t col_capacity, float* block_scores, void* workspace,
-                                     size_t workspace_bytes, void* stream) {
-  g_last_error[0] = 0;
+// Host checks shared by every builder entry point; on success fills the ids
+// per row (nk), the floor k_min and the key scale.
+static chorus_status check_build(chorus_dtype dtype, const chorus_shape* shape, const chorus_tensor* q,
+                                 const float* q_scale, const chorus_tensor* k, const float* k_scale,
+                                 double sm_scale, double top_p, double min_top_k, int32_t kv_block,
+                                 const chorus_key_scale* key_scale, int32_t* row_ptr, int32_t* col_idx,
+                                 int64_t col_capacity, int* nk_out, int* k_min_out, KeyScale* ks_out) {
   chorus_status st;
   if ((st = check_shape(shape))) return st;
   const bool fp8 = dtype == CHORUS_FP8_E4M3;
@@ -187,11 +187,32 @@ static chorus_status build_mask_impl(chorus_dtype dtype, const chorus_shape* sha
   if (col_capacity < rows * nk)
     return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
                 (long long)(rows * nk));
+  *nk_out = nk;
+  *k_min_out = (int)std::ceil(min_top_k * (double)nk - 1e-9);
+  *ks_out = ks;
+  return CHORUS_OK;
+}
+
+static chorus_status build_mask_impl(chorus_dtype dtype, const chorus_shape* shape, const chorus_tensor* q,
+                                     const float* q_scale, const chorus_tensor* k, const float* k_scale,
+                                     double sm_scale, double top_p, double min_top_k, int32_t kv_block,
+                                     const chorus_key_scale* key_scale, int32_t* row_ptr, int32_t* col_idx,
+                                     int64_t col_capacity, float* block_scores, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  int nk = 0, k_min = 0;
+  KeyScale ks;
+  if ((st = check_build(dtype, shape, q, q_scale, k, k_scale, sm_scale, top_p, min_top_k, kv_block, key_scale,
+                        row_ptr, col_idx, col_capacity, &nk, &k_min, &ks)))
+    return st;
+  const bool fp8 = dtype == CHORUS_FP8_E4M3;
+  const int n = blocks_of(shape->S);
+  const int64_t rows = (int64_t)shape->B * shape->H * n;
   size_t need = 0;
   BuilderWorkspace w = carve_builder(workspace, shape->B, shape->H, n, &need);   // sized for nk <= n
   if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
   const int words = (nk + 31) / 32;
-  const int k_min = (int)std::ceil(min_top_k * (double)nk - 1e-9);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const hipError_t pe = fp8 ? launch_pool_fp8(targ(q), q_scale, targ(k), k_scale, shape->B, shape->S, shape->H,
                                               kv_block, ks, w.qbar, w.kbar, s)
@@ -231,6 +252,32 @@ chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const choru
   return build_mask_impl(CHORUS_FP8_E4M3, shape, q, q_scale, k, k_scale, sm_scale, top_p, min_top_k, kv_block,
                          key_scale, row_ptr, col_idx, col_capacity, block_scores, workspace, workspace_bytes,
                          stream);
+}
+
+chorus_status chorus_build_block_mask_noalloc(chorus_dtype dtype, const chorus_shape* shape,
+                                              const chorus_tensor* q, const chorus_tensor* k, double sm_scale,
+                                              double top_p, double min_top_k, int32_t kv_block,
+                                              const chorus_key_scale* key_scale, int32_t* row_ptr,
+                                              int32_t* col_idx, int64_t col_capacity, float* block_scores,
+                                              void* stream) {
+  g_last_error[0] = 0;
+  if (dtype != CHORUS_F16 && dtype != CHORUS_BF16)
+    return fail(CHORUS_ERR_UNSUPPORTED, "builder without allocation takes f16 or bf16 input (dtype %d)", (int)dtype);
+  chorus_status st;
+  int nk = 0, k_min = 0;
+  KeyScale ks;
+  if ((st = check_build(dtype, shape, q, nullptr, k, nullptr, sm_scale, top_p, min_top_k, kv_block, key_scale,
+                        row_ptr, col_idx, col_capacity, &nk, &k_min, &ks)))
+    return st;
+  const int n = blocks_of(shape->S);
+  const int64_t rows = (int64_t)shape->B * shape->H * n;
+  if (noalloc_heads_per_chunk(rows, (nk + 31) / 32, n, nk, shape->H) < 1)
+    return fail(CHORUS_ERR_CAPACITY,
+                "B*H*n_blocks=%lld rows with %d kv blocks need more than the %zu-byte builder scratch "
+                "(counts and bitmaps of every row plus one head's pooled means and scores)",
+                (long long)rows, nk, builder_noalloc_scratch_bytes());
+  return build_mask_noalloc(dtype, shape->B, shape->S, shape->H, targ(q), targ(k), sm_scale, top_p, k_min, kv_block,
+                            ks, row_ptr, col_idx, block_scores, static_cast<hipStream_t>(stream));
 }
 
 size_t chorus_plan_workspace_size(const chorus_shape* shape, const chorus_block_mask* mask) {

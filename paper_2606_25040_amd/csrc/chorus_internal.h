@@ -77,6 +77,13 @@ hipError_t launch_plan(const int32_t* row_ptr, int mask_batch, int B, int H, int
 hipError_t launch_validate(const int32_t* row_ptr, const int32_t* col_idx, int64_t rows, int n,
                            int64_t capacity, int32_t* flags, hipStream_t st);
 
+// ---- mask builder with its scratch in a fixed device array (builder_noalloc.hip) ----
+size_t builder_noalloc_scratch_bytes();
+int noalloc_heads_per_chunk(int64_t rows, int words, int n, int nk, int H);
+chorus_status build_mask_noalloc(chorus_dtype dtype, int B, int S, int H, const TensorArg& q, const TensorArg& k,
+                                 double sm_scale, double top_p, int k_min, int kv_block, KeyScale ks,
+                                 int32_t* row_ptr, int32_t* col_idx, float* block_scores, hipStream_t st);
+
 // ---- block mass and coverage (block_mass.hip) ----
 hipError_t launch_block_mass(chorus_dtype dt, TensorArg q, TensorArg k, const float* lse, int B, int S, int H,
                              float sm_scale, KeyScale ks, int kvb, float* mass, hipStream_t st);

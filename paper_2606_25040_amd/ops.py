@@ -60,6 +60,7 @@ def _key_scale(key_scale):
 
 EXPORTS = [
     "chorus_build_block_mask_workspace_size", "chorus_build_block_mask", "chorus_build_block_mask_fp8",
+    "chorus_build_block_mask_noalloc",
     "chorus_plan_workspace_size", "chorus_plan_block_mask", "chorus_validate_block_mask",
     "chorus_quantize_fp8_blockwise", "chorus_attn_workspace_size",
     "chorus_block_sparse_attn_fwd", "chorus_block_sparse_attn_fwd_f16",
@@ -91,6 +92,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                           P(KeyScale), VP, VP, I64, VP, VP, SZ, VP]),
         "chorus_build_block_mask_fp8": (I32, [P(Shape), P(Tensor), VP, P(Tensor), VP, F64, F64, F64, I32,
                                               P(KeyScale), VP, VP, I64, VP, VP, SZ, VP]),
+        "chorus_build_block_mask_noalloc": (I32, [I32, P(Shape), P(Tensor), P(Tensor), F64, F64, F64, I32,
+                                                  P(KeyScale), VP, VP, I64, VP, VP]),
         "chorus_plan_workspace_size": (SZ, [P(Shape), P(Mask)]),
         "chorus_plan_block_mask": (I32, [P(Shape), P(Mask), VP, VP, SZ, VP]),
         "chorus_validate_block_mask": (I32, [P(Mask), I64, VP, VP]),
@@ -272,6 +275,29 @@ def build_block_mask(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: 
         st = L.chorus_build_block_mask(_dtype_code(q), ctypes.byref(shape), ctypes.byref(_tensor(q)),
                                        ctypes.byref(_tensor(k)), *tail)
         _check(st, "chorus_build_block_mask")
+    return out
+
+
+def build_block_mask_noalloc(q: torch.Tensor, k: torch.Tensor, top_p: float, min_top_k: float, out: BlockMask,
+                             sm_scale: float | None = None, key_scale=None, kv_block: int = BLOCK,
+                             block_scores: torch.Tensor | None = None) -> BlockMask:
+    """chorus_build_block_mask_noalloc: the builder on f16 / bf16 ``q, k`` with
+    the library's own fixed scratch; the caller passes the output mask
+    buffers (``out``, and ``block_scores`` [rows, n_kv] fp32 to receive the
+    scores) so that nothing is allocated."""
+    L = load_library()
+    if q.shape != k.shape or q.dtype != k.dtype:
+        raise ValueError("q and k must share shape and dtype")
+    B, S, H, D = q.shape
+    sm = 1.0 / math.sqrt(D) if sm_scale is None else float(sm_scale)
+    out.block = kv_block
+    out.block_scores = block_scores
+    st = L.chorus_build_block_mask_noalloc(_dtype_code(q), ctypes.byref(_shape(q)), ctypes.byref(_tensor(q)),
+                                           ctypes.byref(_tensor(k)), sm, float(top_p), float(min_top_k),
+                                           int(kv_block), _key_scale(key_scale), out.row_ptr.data_ptr(),
+                                           out.col_idx.data_ptr(), out.col_idx.numel(), _ptr(block_scores),
+                                           _stream())
+    _check(st, "chorus_build_block_mask_noalloc")
     return out
 
 

@@ -78,6 +78,31 @@ def test_builder_argument_checks(lib):
     assert b"stride" in lib.chorus_last_error()
 
 
+def build_noalloc(lib, shp, top_p=0.5, mk=0.1, cap=None, dtype=ops.BF16, kvb=64):
+    n = (shp.S + 63) // 64
+    nk = (shp.S + kvb - 1) // kvb
+    rows = shp.B * shp.H * n
+    cap = rows * nk if cap is None else cap
+    qq = t4(shp.B, shp.S, shp.H)
+    return lib.chorus_build_block_mask_noalloc(dtype, ctypes.byref(shp), ctypes.byref(qq), ctypes.byref(qq),
+                                               0.088, top_p, mk, kvb, None, FAKE, FAKE, cap, None, None)
+
+
+def test_noalloc_builder_rejects_before_any_device_call(lib):
+    """Every rejection happens in the host checks, before the first device
+    call; in particular a shape whose single head does not fit the fixed
+    scratch (n_blocks = 4096: 8.4 MB of pooled means plus 134 MB of scores)
+    is CHORUS_ERR_CAPACITY, and fp8 input is not taken."""
+    assert build_noalloc(lib, shape(S=64 * 4096, H=1)) == 3
+    assert b"scratch" in lib.chorus_last_error()
+    assert build_noalloc(lib, shape(S=64 * 2800, H=1)) == 3
+    assert build_noalloc(lib, shape(), dtype=ops.FP8_E4M3) == 2
+    assert build_noalloc(lib, shape(D=64)) == 2
+    assert build_noalloc(lib, shape(), top_p=1.5) == 1
+    assert build_noalloc(lib, shape(), cap=3) == 3
+    assert build_noalloc(lib, shape(), kvb=96) == 2
+
+
 def attn(lib, shp, mask, dtype=ops.BF16, scales=(None, None, None), sched=None, sm=0.088, ks=None):
     t = t4(shp.B, shp.S, shp.H)
     return lib.chorus_block_sparse_attn_fwd(dtype, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t),
