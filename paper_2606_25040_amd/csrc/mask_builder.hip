@@ -908,15 +908,29 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict
 // least-loaded XCD that still has room (equal unit counts per XCD); the order
 // lists the units XCD by XCD, ascending unit id inside an XCD.  One
 // workgroup, everything in LDS: costs, a rank sort by (cost desc, id asc),
-// then the sequential greedy pass.  Beyond kPlanMaxUnits units the natural
-// order is kept.
+// the greedy pass on one wave (the eight loads live in registers, the sorted
+// costs are read lane by lane, so a step is a few dozen ALU operations), then
+// the placement of every unit in parallel.  Beyond kPlanMaxUnits units the
+// natural order is kept.
 // ---------------------------------------------------------------------------
 constexpr int kPlanMaxUnits = 4096;
+
+// Minimum of a 64-bit value with the value a DPP pattern brings in; lanes the
+// pattern gives no source keep their own.
+template <int kCtrl>
+__device__ inline uint64_t dpp_min_u64(uint64_t v) {
+  const int lo = (int)(uint32_t)v, hi = (int)(uint32_t)(v >> 32);
+  const uint32_t olo = (uint32_t)__builtin_amdgcn_update_dpp(lo, lo, kCtrl, 0xF, 0xF, false);
+  const uint32_t ohi = (uint32_t)__builtin_amdgcn_update_dpp(hi, hi, kCtrl, 0xF, 0xF, false);
+  const uint64_t o = (uint64_t)ohi << 32 | olo;
+  return o < v ? o : v;
+}
 
 __global__ __launch_bounds__(256) void plan_kernel(const int32_t* __restrict__ row_ptr, int mask_batch, int B,
                                                    int H, int n, int per_id, int32_t* __restrict__ order) {
   __shared__ int32_t cost[kPlanMaxUnits];
   __shared__ int32_t by_cost[kPlanMaxUnits];
+  __shared__ int32_t sorted_cost[kPlanMaxUnits];
   __shared__ uint8_t xcd_of[kPlanMaxUnits];
   const int U = B * H;
   const int tid = threadIdx.x;
@@ -938,37 +952,42 @@ __global__ __launch_bounds__(256) void plan_kernel(const int32_t* __restrict__ r
       rank += (cv > cu || (cv == cu && v < u)) ? 1 : 0;
     }
     by_cost[rank] = u;
+    sorted_cost[rank] = cu;
   }
   __syncthreads();
-  if (tid == 0) {
-    int64_t load[kNumXcd];
-    int used[kNumXcd], cap[kNumXcd];
-    for (int x = 0; x < kNumXcd; ++x) {
-      load[x] = 0;
-      used[x] = 0;
-      cap[x] = U / kNumXcd + (x < U % kNumXcd ? 1 : 0);
-    }
-    for (int p = 0; p < U; ++p) {
-      const int u = by_cost[p];
-      int best = -1;
-      for (int x = 0; x < kNumXcd; ++x) {
-        if (used[x] >= cap[x]) continue;
-        if (best < 0 || load[x] < load[best]) best = x;
+  const int base_cap = U / kNumXcd, extra = U % kNumXcd;
+  if (tid < 64) {
+    // Lane x < 8 owns XCD x; its key (load << 3 | x) orders by load, then id,
+    // and a full XCD (or a lane beyond 8) carries the largest key.
+    int64_t load = 0;
+    int left = tid < kNumXcd ? base_cap + (tid < extra ? 1 : 0) : 0;
+    for (int p0 = 0; p0 < U; p0 += 64) {
+      const int mine_p = p0 + tid;
+      const int32_t c_lane = mine_p < U ? sorted_cost[mine_p] : 0;
+      const int steps = U - p0 < 64 ? U - p0 : 64;
+      int mine = 0;
+      for (int j = 0; j < steps; ++j) {
+        const int32_t c = __builtin_amdgcn_readlane(c_lane, j);
+        uint64_t key = left > 0 ? ((uint64_t)load << 3 | (uint64_t)tid) : ~0ull;
+        key = dpp_min_u64<0xB1>(key);   // quad_perm [1,0,3,2]
+        key = dpp_min_u64<0x4E>(key);   // quad_perm [2,3,0,1]
+        key = dpp_min_u64<0x114>(key);  // row_shr:4 -> lanes 4..7 hold the minimum of lanes 0..7
+        const int best = __builtin_amdgcn_readlane((int)(uint32_t)key, 4) & (kNumXcd - 1);
+        load += tid == best ? c : 0;
+        left -= tid == best ? 1 : 0;
+        mine = tid == j ? best : mine;
       }
-      load[best] += cost[u];
-      used[best] += 1;
-      xcd_of[u] = (uint8_t)best;
+      if (mine_p < U) xcd_of[by_cost[mine_p]] = (uint8_t)mine;
     }
-    int start[kNumXcd];
-    int run = 0;
-    for (int x = 0; x < kNumXcd; ++x) {
-      start[x] = run;
-      run += cap[x];
-    }
-    for (int u = 0; u < U; ++u) by_cost[start[xcd_of[u]]++] = u;
   }
   __syncthreads();
-  for (int u = tid; u < U; u += 256) order[u] = by_cost[u];
+  // Unit u lands after every unit of a lower XCD and every lower unit of its own.
+  for (int u = tid; u < U; u += 256) {
+    const int x = xcd_of[u];
+    int pos = x * base_cap + (x < extra ? x : extra);
+    for (int v = 0; v < u; ++v) pos += xcd_of[v] == x ? 1 : 0;
+    order[pos] = u;
+  }
 }
 
 // ---------------------------------------------------------------------------
