@@ -129,15 +129,19 @@ __global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* 
 
 // ---------------------------------------------------------------------------
 // 2a. Block scores s = sm_scale * qbar kbar^T per (request, head), n x nk
-// (q-blocks x kv blocks): a float64 GEMM tile of 128 x 128 outputs per workgroup of 256 threads (8 x 8 outputs
-// per thread, rows ti + 16 a, columns tj + 16 c), the k-dim staged through
-// LDS in chunks of 16.  Writes float64 scores into the workspace and,
-// optionally, fp32 copies.
+// (q-blocks x kv blocks): a float64 GEMM on the matrix cores
+// (v_mfma_f64_16x16x4f64), one 128 x 128 output tile per workgroup of four
+// waves, each wave a 64 x 64 quarter as 4 x 4 MFMA tiles.  The head dim is
+// staged through LDS sixteen at a time (both operands k-major, so a lane's
+// fragment is one float64 of a row); the next chunk is fetched into
+// registers while the current one is multiplied.  Writes float64 scores
+// into the workspace and, optionally, fp32 copies.
 // ---------------------------------------------------------------------------
 constexpr int kST = 128;  // score tile
 constexpr int kSK = 16;   // k-chunk
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ qbar,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void score_kernel(const double* __restrict__ qbar,
                                                     const double* __restrict__ kbar, int n, int nk, double sm_scale,
                                                     double* __restrict__ scores, float* __restrict__ scores32) {
   __shared__ double qs[kSK][kST + 2];
@@ -147,52 +151,72 @@ __global__ __launch_bounds__(256) void score_kernel(const double* __restrict__ q
   const double* qb = qbar + (int64_t)bh * n * kHeadDim;
   const double* kb = kbar + (int64_t)bh * nk * kHeadDim;
   const int tid = threadIdx.x;
-  const int ti = tid / 16, tj = tid % 16;
-  double acc[8][8];
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wr = wave >> 1, wc = wave & 1;
+  const int li = lane & 15, lk = lane >> 4;
+  // staging: thread -> (row r, dims d0 .. d0 + 7) of each operand's chunk
+  const int sr = tid >> 1, sd0 = (tid & 1) * 8;
+  const bool qin = i0 + sr < n, kin = j0 + sr < nk;
+  const double* qrow = qb + (int64_t)(qin ? i0 + sr : 0) * kHeadDim + sd0;
+  const double* krow = kb + (int64_t)(kin ? j0 + sr : 0) * kHeadDim + sd0;
+  double qv[8], kv[8];
 #pragma unroll
-  for (int a = 0; a < 8; ++a)
+  for (int d = 0; d < 8; ++d) {
+    qv[d] = qin ? qrow[d] : 0.0;
+    kv[d] = kin ? krow[d] : 0.0;
+  }
+  f64x4 acc[4][4];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) acc[a][c] = 0.0;
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[a][c] = (f64x4){0.0, 0.0, 0.0, 0.0};
   for (int kk = 0; kk < kHeadDim; kk += kSK) {
-    // 128 rows x 16 dims of each operand: thread -> (row, 8-dim half) pairs
-    for (int e = tid; e < kST * 2; e += 256) {
-      const int r = e >> 1, d0 = (e & 1) * 8;
-      const bool qin = i0 + r < n, kin = j0 + r < nk;
+    __syncthreads();   // the previous chunk is no longer read
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      qs[sd0 + d][sr] = qv[d];
+      ks[sd0 + d][sr] = kv[d];
+    }
+    __syncthreads();
+    if (kk + kSK < kHeadDim) {
 #pragma unroll
       for (int d = 0; d < 8; ++d) {
-        qs[d0 + d][r] = qin ? qb[(int64_t)(i0 + r) * kHeadDim + kk + d0 + d] : 0.0;
-        ks[d0 + d][r] = kin ? kb[(int64_t)(j0 + r) * kHeadDim + kk + d0 + d] : 0.0;
+        qv[d] = qin ? qrow[kk + kSK + d] : 0.0;
+        kv[d] = kin ? krow[kk + kSK + d] : 0.0;
       }
     }
-    __syncthreads();
-#pragma unroll 4
-    for (int d = 0; d < kSK; ++d) {
-      double qa[8], kc[8];
 #pragma unroll
-      for (int a = 0; a < 8; ++a) qa[a] = qs[d][ti + 16 * a];
+    for (int k4 = 0; k4 < kSK; k4 += 4) {
+      // A[i][k]: lane holds row i = li of the tile, k = lk; B[k][j]: column j = li
+      double af[4], bf[4];
 #pragma unroll
-      for (int c = 0; c < 8; ++c) kc[c] = ks[d][tj + 16 * c];
+      for (int t = 0; t < 4; ++t) {
+        af[t] = qs[k4 + lk][wr * 64 + t * 16 + li];
+        bf[t] = ks[k4 + lk][wc * 64 + t * 16 + li];
+      }
 #pragma unroll
-      for (int a = 0; a < 8; ++a)
+      for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int c = 0; c < 8; ++c) acc[a][c] = fma(qa[a], kc[c], acc[a][c]);
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int a = 0; a < 8; ++a) {
-    const int i = i0 + ti + 16 * a;
-    if (i >= n) continue;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int j = j0 + tj + 16 * c;
-      if (j >= nk) continue;
-      const double v = sm_scale * acc[a][c];
-      const int64_t o = ((int64_t)bh * n + i) * nk + j;
-      scores[o] = v;
-      if (scores32) scores32[o] = (float)v;
+        for (int c = 0; c < 4; ++c) acc[a][c] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[a], bf[c], acc[a][c], 0, 0, 0);
     }
   }
+  // D tile element (4 r + lane / 16, lane % 16) sits in register r of the lane
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = i0 + wr * 64 + a * 16 + 4 * r + lk;
+      if (i >= n) continue;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int j = j0 + wc * 64 + c * 16 + li;
+        if (j >= nk) continue;
+        const double v = sm_scale * acc[a][c][r];
+        const int64_t o = ((int64_t)bh * n + i) * nk + j;
+        scores[o] = v;
+        if (scores32) scores32[o] = (float)v;
+      }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -570,11 +594,14 @@ __device__ inline T wave_bcast(T v, int src) {
 }
 
 template <int PER, bool FROM_MASS>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ? 4 : 2))) void select_wave_kernel(const void* __restrict__ in, int n, int64_t rows,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ? 4 : PER <= 24 ? 2 : 1))) void select_wave_kernel(const void* __restrict__ in, int n, int64_t rows,
                                                           double top_p, int k_min, int32_t* __restrict__ counts,
                                                           uint32_t* __restrict__ bitmap, int words) {
   __shared__ uint32_t hist_cnt_all[4][256];
   __shared__ uint64_t hist_mass_all[4][256];
+  __shared__ uint64_t cand_key_all[4][64];
+  __shared__ uint64_t cand_mass_all[4][64];
+  __shared__ int32_t cand_idx_all[4][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + wave;
   if (row >= rows) return;
@@ -586,17 +613,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
   };
 
   uint64_t key[PER], mass[PER];
-  double m = -INFINITY;
+  uint32_t binw[(PER + 3) / 4];   // 8-bit value bins, four per word
+  double m = -INFINITY, mn = INFINITY;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
     const double v = j < n ? value(j) : -INFINITY;
     key[e] = (uint64_t)__double_as_longlong(v);
     m = fmax(m, v);
+    if (j < n) mn = fmin(mn, v);
   }
-  if (!FROM_MASS)
-    for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+  for (int o = 32; o > 0; o >>= 1) {
+    m = fmax(m, __shfl_xor(m, o));
+    mn = fmin(mn, __shfl_xor(mn, o));
+  }
+  // value bins: floor((v - min) * 255.5 / (max - min)), non-decreasing in v,
+  // so every block of a higher bin comes before every block of a lower one
+  const double bscale = m > mn ? 255.5 / (m - mn) : 0.0;
   double z = 0.0;
+#pragma unroll
+  for (int e = 0; e < (PER + 3) / 4; ++e) binw[e] = 0u;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
@@ -604,30 +640,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
     const double x = j < n ? (FROM_MASS ? v : exp(v - m)) : 0.0;
     mass[e] = (uint64_t)__double_as_longlong(x);
     z += x;
+    if (j < n) {
+      const uint32_t bin = (uint32_t)((v - mn) * bscale);
+      binw[e >> 2] |= (bin > 255u ? 255u : bin) << (8 * (e & 3));
+    }
+    key[e] = j < n ? order_key(v) : 0;
   }
   for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o);
-  uint64_t total = 0, kmin = ~0ull, kmax = 0;
+  // block masses as 62-bit fixed point: round(x * 2^62 / z)
+  const double to_fixed = z > 0.0 ? kMassOne / z : 0.0;
+  uint64_t total = 0;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
-    if (j < n) {
-      const double share = z > 0.0 ? __longlong_as_double((long long)mass[e]) / z : 0.0;
-      mass[e] = __double2ull_rn(share * kMassOne);
-      key[e] = order_key(__longlong_as_double((long long)key[e]));
-      kmin = key[e] < kmin ? key[e] : kmin;
-      kmax = key[e] > kmax ? key[e] : kmax;
-    } else {
-      mass[e] = 0;
-      key[e] = 0;
-    }
+    mass[e] = j < n ? __double2ull_rn(__longlong_as_double((long long)mass[e]) * to_fixed) : 0;
     total += mass[e];
   }
-  for (int o = 32; o > 0; o >>= 1) {
-    total += __shfl_xor(total, o);
-    const uint64_t a = __shfl_xor(kmin, o), b = __shfl_xor(kmax, o);
-    kmin = a < kmin ? a : kmin;
-    kmax = b > kmax ? b : kmax;
-  }
+  for (int o = 32; o > 0; o >>= 1) total += __shfl_xor(total, o);
 
   SelCond cond;
   cond.any_mass = !(top_p > 0.0);
@@ -638,7 +667,142 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
   uint64_t kb = 0;   // keep blocks with key > kb, and key == kb with index <= jb
   int jb = n;
   uint32_t k = (uint32_t)n;
+  bool found = false;
   if (!keep_all) {
+    // Histogram of (count, mass) over the value bins, scanned from the top:
+    // the first bin whose cumulative (count, mass) meets both conditions holds
+    // the boundary block.
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      hist_cnt[4 * lane + q] = 0u;
+      hist_mass[4 * lane + q] = 0ull;
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int j = lane + 64 * e;
+      if (j < n) {
+        const int bin = (int)((binw[e >> 2] >> (8 * (e & 3))) & 255u);
+        atomicAdd(&hist_cnt[bin], 1u);
+        atomicAdd((unsigned long long*)&hist_mass[bin], (unsigned long long)mass[e]);
+      }
+    }
+    wave_lds_sync();
+    uint32_t c[4], c4 = 0;
+    uint64_t ms[4], m4 = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      c[q] = hist_cnt[4 * lane + q];
+      ms[q] = hist_mass[4 * lane + q];
+      c4 += c[q];
+      m4 += ms[q];
+    }
+    uint32_t cs = c4;
+    uint64_t msum = m4;
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t vc = __shfl_down(cs, o);
+      const uint64_t vm = __shfl_down(msum, o);
+      if (lane + o < 64) {
+        cs += vc;
+        msum += vm;
+      }
+    }
+    uint32_t cc = cs - c4;
+    uint64_t mm = msum - m4;
+    bool before = cond(cc, mm);
+    int f_bin = -1;
+    uint32_t f_cnt_above = 0, f_bin_cnt = 0;
+    uint64_t f_mass_above = 0;
+#pragma unroll
+    for (int q = 3; q >= 0; --q) {
+      const uint32_t c2 = cc + c[q];
+      const uint64_t m2 = mm + ms[q];
+      const bool now = cond(c2, m2);
+      if (now && !before) {
+        f_bin = 4 * lane + q;
+        f_cnt_above = cc;
+        f_mass_above = mm;
+        f_bin_cnt = c[q];
+      }
+      before = now;
+      cc = c2;
+      mm = m2;
+    }
+    const int src = __ffsll((long long)__builtin_amdgcn_ballot_w64(f_bin >= 0)) - 1;
+    const int bin_b = wave_bcast(f_bin, src);
+    const uint32_t cnt_b = wave_bcast(f_cnt_above, src);
+    const uint64_t mass_b = wave_bcast(f_mass_above, src);
+    const uint32_t n_cand = wave_bcast(f_bin_cnt, src);
+    wave_lds_sync();
+    if (src >= 0 && n_cand <= 64) {
+      // The bin's blocks, one per lane, ranked by (key descending, index
+      // ascending); the boundary is the first of them, in that order, at which
+      // both conditions hold.
+      uint64_t* ck = cand_key_all[wave];
+      uint64_t* cm = cand_mass_all[wave];
+      int32_t* cj = cand_idx_all[wave];
+      uint32_t at = 0;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const int j = lane + 64 * e;
+        const bool is_c = j < n && (int)((binw[e >> 2] >> (8 * (e & 3))) & 255u) == bin_b;
+        const uint64_t bm = __builtin_amdgcn_ballot_w64(is_c);
+        if (is_c) {
+          const uint32_t pos = at + (uint32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(bm >> 32),
+                                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)bm, 0u));
+          ck[pos] = key[e];
+          cm[pos] = mass[e];
+          cj[pos] = j;
+        }
+        at += (uint32_t)__popcll(bm);
+      }
+      wave_lds_sync();
+      const bool mine = (uint32_t)lane < n_cand;
+      const uint64_t my_k = mine ? ck[lane] : 0;
+      const uint64_t my_m = mine ? cm[lane] : 0;
+      const int my_j = mine ? cj[lane] : 0;
+      uint32_t rank = 0;
+      uint64_t cum = 0;
+      for (uint32_t t = 0; t < n_cand; ++t) {
+        const uint64_t kt = ck[t];
+        const int jt = cj[t];
+        const bool pre = kt > my_k || (kt == my_k && jt < my_j);
+        rank += pre ? 1u : 0u;
+        cum += pre ? cm[t] : 0ull;
+      }
+      wave_lds_sync();
+      const bool ok = mine && cond(cnt_b + rank + 1, mass_b + cum + my_m);
+      uint32_t r_min = ok ? rank : 0xffffffffu;
+      for (int o = 32; o > 0; o >>= 1) {
+        const uint32_t w = __shfl_xor(r_min, o);
+        r_min = w < r_min ? w : r_min;
+      }
+      const int src2 = __ffsll((long long)__builtin_amdgcn_ballot_w64(ok && rank == r_min)) - 1;
+      if (src2 >= 0) {
+        kb = wave_bcast(my_k, src2);
+        jb = wave_bcast(my_j, src2);
+        k = cnt_b + r_min + 1;
+        found = true;
+      }
+    }
+  }
+  if (!keep_all && !found) {
+    // Fallback: radix descent over the order keys (a bin holding more than 64
+    // blocks).
+    uint64_t kmin = ~0ull, kmax = 0;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int j = lane + 64 * e;
+      if (j < n) {
+        kmin = key[e] < kmin ? key[e] : kmin;
+        kmax = key[e] > kmax ? key[e] : kmax;
+      }
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint64_t a = __shfl_xor(kmin, o), b = __shfl_xor(kmax, o);
+      kmin = a < kmin ? a : kmin;
+      kmax = b > kmax ? b : kmax;
+    }
     const uint64_t diff = kmin ^ kmax;
     int lo = diff ? 64 - __clzll((long long)diff) : 0;
     uint64_t prefix = lo == 64 ? 0 : (kmin >> lo) << lo;
