@@ -70,15 +70,6 @@ __global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int 
   }
 }
 
-// OCP e4m3fn code -> float, exactly: bias 7, three mantissa bits, subnormals
-// m * 2^-9, S.1111.111 is NaN, no infinities.
-__device__ inline float e4m3_to_f32(uint32_t c) {
-  const uint32_t e = (c >> 3) & 15u, m = c & 7u;
-  float mag = e == 0 ? (float)m * 0x1p-9f : __uint_as_float(((e + 120u) << 23) | (m << 20));
-  if (e == 15u && m == 7u) mag = __builtin_nanf("");
-  return (c & 0x80u) ? -mag : mag;
-}
-
 // 1b. Block mean-pool of fp8 e4m3 codes with per-(request, head, 64-token
 // block) scales, as written by the fp8 quantiser: the mean of code * scale
 // over the block's valid tokens, in float64.  Same lane layout as
@@ -109,11 +100,16 @@ __global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* 
     const uint2 raw = *reinterpret_cast<const uint2*>(base + (int64_t)(t0 + tok) * t.ss);
     // the token's value is code * (scale of its 64-token block)
     const double wt = (t0 + tok < n_scaled ? beta : 1.0) * (double)sc[(t0 + tok) / kBlock];
+    // v_cvt_pk_f32_fp8 decodes OCP e4m3fn exactly: each of the 256 codes gives
+    // the value of its fields (bias 7, three mantissa bits, subnormals
+    // m * 2^-9, S.1111.111 NaN)
+    const auto f01 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw.x, false);
+    const auto f23 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw.x, true);
+    const auto f45 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw.y, false);
+    const auto f67 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw.y, true);
+    const float f[8] = {f01[0], f01[1], f23[0], f23[1], f45[0], f45[1], f67[0], f67[1]};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t word = e < 4 ? raw.x : raw.y;
-      acc[e] = __builtin_fma(wt, (double)e4m3_to_f32((word >> (8 * (e & 3))) & 0xffu), acc[e]);
-    }
+    for (int e = 0; e < 8; ++e) acc[e] = __builtin_fma(wt, (double)f[e], acc[e]);
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -154,6 +150,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void s
   const int wave = tid >> 6, lane = tid & 63;
   const int wr = wave >> 1, wc = wave & 1;
   const int li = lane & 15, lk = lane >> 4;
+  const bool wave_live = i0 + wr * 64 < n && j0 + wc * 64 < nk;
   // staging: thread -> (row r, dims d0 .. d0 + 7) of each operand's chunk
   const int sr = tid >> 1, sd0 = (tid & 1) * 8;
   const bool qin = i0 + sr < n, kin = j0 + sr < nk;
@@ -185,8 +182,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void s
         kv[d] = kin ? krow[kk + kSK + d] : 0.0;
       }
     }
+    // a wave whose 64 rows or 64 columns all lie past the matrix edge only
+    // helps stage the operands
 #pragma unroll
-    for (int k4 = 0; k4 < kSK; k4 += 4) {
+    for (int k4 = 0; k4 < (wave_live ? kSK : 0); k4 += 4) {
       // A[i][k]: lane holds row i = li of the tile, k = lk; B[k][j]: column j = li
       double af[4], bf[4];
 #pragma unroll
@@ -637,7 +636,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
     const double v = __longlong_as_double((long long)key[e]);
-    const double x = j < n ? (FROM_MASS ? v : exp(v - m)) : 0.0;
+    double x = 0.0;
+    if (j < n) x = FROM_MASS ? v : exp(v - m);
     mass[e] = (uint64_t)__double_as_longlong(x);
     z += x;
     if (j < n) {
@@ -1220,6 +1220,9 @@ hipError_t launch_select(const void* in, int64_t rows, int n, double top_p, int 
                        counts, bitmap, words);
   } else if (n <= 64 * 16) {
     hipLaunchKernelGGL((select_wave_kernel<16, FROM_MASS>), wave_grid, wave_block, 0, st, in, n, rows, top_p, k_min,
+                       counts, bitmap, words);
+  } else if (n <= 64 * 20) {
+    hipLaunchKernelGGL((select_wave_kernel<20, FROM_MASS>), wave_grid, wave_block, 0, st, in, n, rows, top_p, k_min,
                        counts, bitmap, words);
   } else if (n <= 64 * 24) {
     hipLaunchKernelGGL((select_wave_kernel<24, FROM_MASS>), wave_grid, wave_block, 0, st, in, n, rows, top_p, k_min,
