@@ -183,23 +183,46 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void s
       }
     }
     // a wave whose 64 rows or 64 columns all lie past the matrix edge only
-    // helps stage the operands
-#pragma unroll
-    for (int k4 = 0; k4 < (wave_live ? kSK : 0); k4 += 4) {
-      // A[i][k]: lane holds row i = li of the tile, k = lk; B[k][j]: column j = li
-      double af[4], bf[4];
+    // helps stage the operands.  A[i][k]: lane holds row i = li of the tile,
+    // k = lk; B[k][j]: column j = li.  The fragments of the next k-step are
+    // read while this step's 16 products run.
+    if (wave_live) {
+      double af[2][4], bf[2][4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        af[t] = qs[k4 + lk][wr * 64 + t * 16 + li];
-        bf[t] = ks[k4 + lk][wc * 64 + t * 16 + li];
+        af[0][t] = qs[lk][wr * 64 + t * 16 + li];
+        bf[0][t] = ks[lk][wc * 64 + t * 16 + li];
       }
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int k4 = 0; k4 < kSK; k4 += 4) {
+        const int cur = (k4 / 4) & 1;
+        if (k4 + 4 < kSK) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[a][c] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[a], bf[c], acc[a][c], 0, 0, 0);
+          for (int t = 0; t < 4; ++t) {
+            af[cur ^ 1][t] = qs[k4 + 4 + lk][wr * 64 + t * 16 + li];
+            bf[cur ^ 1][t] = ks[k4 + 4 + lk][wc * 64 + t * 16 + li];
+          }
+        }
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            acc[a][c] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[cur][a], bf[cur][c], acc[a][c], 0, 0, 0);
+      }
     }
   }
   // D tile element (4 r + lane / 16, lane % 16) sits in register r of the lane
+  if (i0 + kST <= n && j0 + kST <= nk && !scores32) {
+    // interior tile, float64 scores only: no per-element checks
+    double* out = scores + ((int64_t)bh * n + i0 + wr * 64 + lk) * nk + j0 + wc * 64 + li;
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) out[(int64_t)(a * 16 + 4 * r) * nk + c * 16] = sm_scale * acc[a][c][r];
+    return;
+  }
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
