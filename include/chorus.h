@@ -217,16 +217,18 @@ chorus_status chorus_build_block_mask_noalloc(chorus_dtype dtype, const chorus_s
  * (Sec. 3.2 "Head-level scheduling for load balancing", Appendix A): because
  * a reused mask's per-head cost is known before the attention runs, heads can
  * be placed ahead of time.  The attention kernels deal their work items
- * (q-blocks, in the given unit order) to the 8 XCDs of the GPU as 8 equal
- * contiguous runs; with B * H a multiple of 8 every run is B * H / 8 whole
- * (request, head) units, and the plan orders the units so that those runs
- * carry near-equal cost: units are taken heaviest first (cost = listed
- * 64-token kv blocks + q-blocks, a kv block of 128 counting twice) and each
- * goes to the least-loaded XCD that still has room, the paper's greedy rule
- * with the XCDs in the role of the GPUs.  Within an XCD units keep ascending
- * id, so the workgroups running together share one head's K/V in that XCD's
- * L2.  Otherwise the runs cut through units (so that fewer than 8 units
- * still occupy every XCD) and the plan's balance is approximate.
+ * (q-blocks, in the given unit order) to the 8 XCDs of the GPU as 8
+ * contiguous runs of whole (request, head) units: with U = B * H >= 8 units,
+ * XCD x takes U / 8 units (one more for the first U % 8 XCDs) in turn from
+ * the order.  The plan orders the units so that those runs carry near-equal
+ * cost: units are taken heaviest first (cost = listed 64-token kv blocks +
+ * q-blocks, a kv block of 128 counting twice) and each goes to the
+ * least-loaded XCD that still has room, the paper's greedy rule with the
+ * XCDs in the role of the GPUs, and the order lists the XCDs' units one XCD
+ * after the other.  Within an XCD units keep ascending id, so the workgroups
+ * running together share one head's K/V in that XCD's L2.  With fewer than 8
+ * units the runs are equal runs of q-blocks that cut through units, so that
+ * every XCD still gets work.
  * Computed on device, once per mask, and reusable for every call that applies
  * the same mask to B requests.
  *

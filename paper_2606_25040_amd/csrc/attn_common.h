@@ -46,23 +46,33 @@ __device__ inline float pair_sum(float v) {
 // `np` per (request, head) unit, numbered unit * np + index, listed in the
 // unit order (the planned order of (request, head) units, or the natural
 // one).  Slots are dealt round-robin to the 8 XCDs, so slot p runs on XCD
-// x = p % 8 as its (p / 8)-th slot there; XCD x walks item positions
-// [x * chunk, (x + 1) * chunk), chunk = ceil(U * np / 8), so all eight XCDs
-// share the work even when there are fewer than eight units.  When U is a
-// multiple of 8 each XCD's positions are exactly U / 8 whole units, the
-// runs the plan balances.  Returns -1 for idle slots.
+// x = p % 8 as its (p / 8)-th slot there.  With U >= 8 units XCD x walks the
+// items of units [s_x, s_x + c_x) of the order, c_x = U / 8 (+1 for the first
+// U % 8 XCDs) and s_x the sum of the earlier c: exactly the groups the plan
+// balances, listed XCD by XCD.  With fewer units than XCDs whole units would
+// leave XCDs idle, so XCD x walks item positions [x * chunk, (x + 1) * chunk),
+// chunk = ceil(U * np / 8), instead.  Returns -1 for idle slots.
 __device__ inline int work_item(const int32_t* order, int U, int np) {
   const int p = blockIdx.x;
-  const int W = U * np;
-  const int chunk = (W + kNumXcd - 1) / kNumXcd;
   const int x = p % kNumXcd, k = p / kNumXcd;
-  const int pos = x * chunk + k;
-  if (k >= chunk || pos >= W) return -1;
+  int pos;
+  if (U >= kNumXcd) {
+    const int base = U / kNumXcd, extra = U % kNumXcd;
+    const int cnt = (base + (x < extra ? 1 : 0)) * np;
+    if (k >= cnt) return -1;
+    pos = (x * base + (x < extra ? x : extra)) * np + k;
+  } else {
+    const int W = U * np;
+    const int chunk = (W + kNumXcd - 1) / kNumXcd;
+    pos = x * chunk + k;
+    if (k >= chunk || pos >= W) return -1;
+  }
   const int unit = order ? order[pos / np] : pos / np;
   return (unit >= 0 && unit < U) ? unit * np + pos % np : -1;
 }
 inline unsigned work_grid(int U, int np) {
-  return (unsigned)(kNumXcd * ((U * np + kNumXcd - 1) / kNumXcd));
+  const int per_xcd = U >= kNumXcd ? (U + kNumXcd - 1) / kNumXcd * np : (U * np + kNumXcd - 1) / kNumXcd;
+  return (unsigned)(kNumXcd * per_xcd);
 }
 
 // One global -> LDS direct load (16 bytes per lane, lane-linear destination
