@@ -341,6 +341,20 @@ def test_plan_follows_greedy_rule(B, H, mask_batch):
     assert order == greedy_plan(rp, B, H, n, mask_batch)
 
 
+@pytest.mark.parametrize("B,H", [(1, 24), (2, 13), (1, 5)])
+def test_plan_equal_costs_follow_the_tie_rules(B, H):
+    # every unit lists every block: all costs equal, so only the tie rules
+    # (units by id, XCDs by id on equal load) decide the order
+    n = 6
+    rows = H * n
+    rp = np.arange(0, rows * n + 1, n, dtype=np.int64)
+    ci = np.tile(np.arange(n), rows)
+    mask = ops.BlockMask.from_host(rp, ci, 1, H, n)
+    order = ops.plan_block_mask(mask, B, 64 * n).cpu().tolist()
+    assert order == greedy_plan(rp, B, H, n, 1)
+    assert sorted(order) == list(range(B * H))
+
+
 def test_attention_fp8_small_full():
     gen = torch.Generator().manual_seed(21)
     B, S, H = 2, 1000, 3
