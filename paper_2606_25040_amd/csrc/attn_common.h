@@ -75,6 +75,34 @@ inline unsigned work_grid(int U, int np) {
   return (unsigned)(kNumXcd * per_xcd);
 }
 
+// Starting point of a q-block's kv walk.  The workgroups an XCD runs at one
+// time hold about 128 neighbouring q-blocks, whose lists share most of their
+// kv blocks; walked from the lowest id they drift apart, because each one
+// starts when an earlier one ends.  Starting q-block i at its first listed
+// block with id >= (i n / kRotDiv) mod n and wrapping round moves the start
+// along with the dispatch, so the workgroups in flight read nearly the same
+// kv blocks at the same time and more of those reads hit the XCD's L2.  The
+// rotation changes only the order in which a row's blocks are accumulated.
+constexpr int kRotDiv = 192;
+__device__ inline int walk_target(int i, int n) { return (int)((int64_t)i * n / kRotDiv % n); }
+
+// Offset in [0, p1 - p0) of the first position p of [p0, p1) whose id(p)
+// reaches `target` (ids ascending), 0 when none does: the rotation of the
+// walk over [p0, p1).  Any other id order still gives a rotation, so every
+// position is visited once whatever the row holds.
+template <class F>
+__device__ inline int walk_rotation(int p0, int p1, int target, F id) {
+  int lo = p0, hi = p1;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (id(mid) < target)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo == p1 ? 0 : lo - p0;
+}
+
 // One global -> LDS direct load (16 bytes per lane, lane-linear destination
 // at `lds`, a wave-uniform LDS byte address).  The LDS address travels in
 // m0; the statement saves m0 to a scratch SGPR, sets it, waits the one wait
@@ -101,67 +129,81 @@ __device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
 // Wait until at most n vector-memory loads of this wave are outstanding.
 #define CHORUS_WAIT_VMCNT(n) asm volatile("s_waitcnt vmcnt(" #n ")" ::: "memory")
 
-// Walk of the merged kv lists of the two q-blocks (2p, 2p + 1) of a pair in
-// ascending kv id, skipping ids outside [0, n).  All lanes hold the same
-// state (it lives in scalar registers).  KV2: the lists hold kv blocks of 128
-// tokens and the walk visits both 64-token halves of each (positions of the
-// doubled list), so ids stay in 64-token units.
+// Walk of the merged kv lists of the two q-blocks (2p, 2p + 1) of a pair,
+// skipping ids outside [0, n).  Each list is walked from its rotated start
+// (walk_target of q-block 2p, the same target for both), and the merge takes
+// the smaller of the two heads in that rotated order, key (id - target) mod n,
+// so a block both lists hold is visited once.  All lanes hold the same state
+// (it lives in scalar registers).  KV2: the lists hold kv blocks of 128 tokens
+// and the walk visits both 64-token halves of each (positions of the doubled
+// list), so ids stay in 64-token units.
 template <bool KV2>
 struct PairWalk {
   ConstI32* col;
-  int pa, a1, pb, b1, n;
+  int a0, la, ra, ca;   // list A: first position, length, rotation, steps taken
+  int b0, lb, rb, cb;
+  int n, target;
   bool dense;
   __device__ void init(const AttnArgs& a, bool is_dense, int b, int h, int ip) {
     col = as_constant(a.col_idx);
     n = a.n;
     dense = is_dense;
     const int ia = 2 * ip, ib = 2 * ip + 1;
+    target = walk_target(ia, n);
     if (dense) {
-      pa = 0;
-      a1 = n;
-      pb = 0;
-      b1 = ib < n ? n : 0;
+      a0 = 0;
+      la = n;
+      b0 = 0;
+      lb = ib < n ? n : 0;
     } else {
       const int64_t r0 = ((int64_t)(a.mask_batch > 1 ? b : 0) * a.H + h) * n;
-      pa = a.row_ptr[r0 + ia];
-      a1 = a.row_ptr[r0 + ia + 1];
-      pb = ib < n ? a.row_ptr[r0 + ib] : 0;
-      b1 = ib < n ? a.row_ptr[r0 + ib + 1] : 0;
+      a0 = a.row_ptr[r0 + ia];
+      la = a.row_ptr[r0 + ia + 1] - a0;
+      b0 = ib < n ? a.row_ptr[r0 + ib] : 0;
+      lb = ib < n ? a.row_ptr[r0 + ib + 1] - b0 : 0;
       if (KV2) {
-        pa *= 2;
-        a1 *= 2;
-        pb *= 2;
-        b1 *= 2;
+        a0 *= 2;
+        la *= 2;
+        b0 *= 2;
+        lb *= 2;
       }
     }
+    auto id = [&](int p) { return id_at(p); };
+    ra = walk_rotation(a0, a0 + la, target, id);
+    rb = walk_rotation(b0, b0 + lb, target, id);
+    ca = cb = 0;
   }
-  __device__ bool listed(int sel) const { return sel == 0 ? a1 > pa : b1 > pb; }
+  __device__ bool listed(int sel) const { return sel == 0 ? la > 0 : lb > 0; }
   __device__ int id_at(int p) const { return dense ? p : KV2 ? 2 * col[p >> 1] + (p & 1) : col[p]; }
+  __device__ int pos_a() const { const int p = ra + ca; return a0 + (p >= la ? p - la : p); }
+  __device__ int pos_b() const { const int p = rb + cb; return b0 + (p >= lb ? p - lb : p); }
   __device__ int head_a() {
-    while (pa < a1) {
-      const int j = id_at(pa);
+    while (ca < la) {
+      const int j = id_at(pos_a());
       if (j >= 0 && j < n) return j;
-      ++pa;
+      ++ca;
     }
     return INT32_MAX;
   }
   __device__ int head_b() {
-    while (pb < b1) {
-      const int j = id_at(pb);
+    while (cb < lb) {
+      const int j = id_at(pos_b());
       if (j >= 0 && j < n) return j;
-      ++pb;
+      ++cb;
     }
     return INT32_MAX;
   }
+  __device__ int key(int j) const { return j == INT32_MAX ? INT32_MAX : j >= target ? j - target : j - target + n; }
   // next kv block of the union (INT32_MAX when done) and which q-blocks list it
   __device__ int next(bool& in_a, bool& in_b) {
     const int ja = head_a(), jb = head_b();
-    const int j = min(ja, jb);
-    in_a = ja == j && j != INT32_MAX;
-    in_b = jb == j && j != INT32_MAX;
-    if (in_a) ++pa;
-    if (in_b) ++pb;
-    return j;
+    const int ka = key(ja), kb = key(jb);
+    const int k = min(ka, kb);
+    in_a = ka == k && k != INT32_MAX;
+    in_b = kb == k && k != INT32_MAX;
+    if (in_a) ++ca;
+    if (in_b) ++cb;
+    return in_a ? ja : jb;
   }
 };
 

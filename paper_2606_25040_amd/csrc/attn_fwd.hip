@@ -4,6 +4,8 @@
 // One workgroup = one work item (request b, head h, 64-query block i), two
 // waves of 32 queries, 32 KB of LDS, so four workgroups (two waves per SIMD)
 // share a CU and hide each other's latencies.  For each listed kv block j:
+//   * the list is walked from a rotated start (walk_target), so the q-blocks
+//     in flight on an XCD read about the same kv blocks at the same time;
 //   * K_j and V_j go global -> LDS with global_load_lds_dwordx4 (no register
 //     staging); each tile has its own single buffer, refilled as soon as the
 //     phase that reads it is over (K after QK^T, V after PV), so the next
@@ -143,11 +145,18 @@ void attn_fwd_16_kernel(AttnArgs a) {
     }
   }
   ConstI32* cidx = as_constant(a.col_idx);   // scalar loads
-  auto kv_block = [&](int jj) { return DENSE ? jj : KV2 ? 2 * cidx[jj >> 1] + (jj & 1) : cidx[jj]; };
+  auto kv_at = [&](int p) { return DENSE ? p : KV2 ? 2 * cidx[p >> 1] + (p & 1) : cidx[p]; };
+  // walk step v visits list position kb0 + (v + rot) mod L (see walk_target)
+  const int L = kb1 - kb0;
+  const int rot = walk_rotation(kb0, kb1, walk_target(i, n), kv_at);
+  auto kv_block = [&](int v) {
+    const int p = v + rot;
+    return kv_at(kb0 + (p >= L ? p - L : p));
+  };
   // ids outside [0, n) are skipped (the builder never emits them; with KV2
   // this also drops the missing half of a last block of 64 tokens)
   auto next_valid = [&](int jj) {
-    while (jj < kb1) {
+    while (jj < L) {
       const int j = kv_block(jj);
       if (j >= 0 && j < n) break;
       ++jj;
@@ -167,8 +176,8 @@ void attn_fwd_16_kernel(AttnArgs a) {
   TileLoader kl, vl;
   kl.init<true>(kbase, a.k.ss, wave, lane);
   vl.init<false>(vbase, a.v.ss, wave, lane);
-  int jj = next_valid(kb0);
-  if (jj < kb1) {
+  int jj = next_valid(0);
+  if (jj < L) {
     const int j0 = kv_block(jj);
     kl.load<true>(k_s, j0, S, wave);
     vl.load<false>(v_s, j0, S, wave);
@@ -209,10 +218,10 @@ void attn_fwd_16_kernel(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[u][r] = 0.f;
 
-  while (jj < kb1) {
+  while (jj < L) {
     const int j = kv_block(jj);
     const int jn = next_valid(jj + 1);
-    const bool has_next = jn < kb1;
+    const bool has_next = jn < L;
     const int j_next = has_next ? kv_block(jn) : 0;
 
     // K_j resident: at most this block's V loads (8) are still in flight

@@ -3,7 +3,8 @@
 //
 // Same work decomposition as the 16-bit kernel: a workgroup takes a pair of
 // neighbouring q-blocks of one (request, head), four waves of 32 queries,
-// walks the union of the two kv lists, and double-buffers the 8 KB K and V
+// walks the union of the two kv lists (from the rotated start of the pair,
+// see walk_target), and double-buffers the 8 KB K and V
 // code tiles in LDS (direct global -> LDS loads, one barrier per kv block).
 // Both products use v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales:
 //   * S^T = K_j Q^T on codes; the true logit is acc * s_q,i * s_k,j * sm_scale,
@@ -116,9 +117,9 @@ void attn_fwd_fp8_kernel(AttnArgs a, int np) {
   // reference V scale: the largest among the pair's listed blocks
   float sref = 0.f;
   {
-    const int la = walk.a1 - walk.pa;
-    for (int t = tid; t < la + (walk.b1 - walk.pb); t += 64 * kWaves) {
-      const int j = t < la ? walk.id_at(walk.pa + t) : walk.id_at(walk.pb + t - la);
+    const int la = walk.la;
+    for (int t = tid; t < la + walk.lb; t += 64 * kWaves) {
+      const int j = t < la ? walk.id_at(walk.a0 + t) : walk.id_at(walk.b0 + t - la);
       if (j >= 0 && j < n) sref = fmaxf(sref, vsc[j]);
     }
     for (int o = 32; o > 0; o >>= 1) sref = fmaxf(sref, __shfl_xor(sref, o));
