@@ -83,6 +83,8 @@ inline unsigned work_grid(int U, int np) {
 // along with the dispatch, so the workgroups in flight read nearly the same
 // kv blocks at the same time and more of those reads hit the XCD's L2.  The
 // rotation changes only the order in which a row's blocks are accumulated.
+// Dense attention (no mask) keeps the natural order: there every q-block
+// lists every block, and starting all of them at block 0 shares more.
 constexpr int kRotDiv = 192;
 __device__ inline int walk_target(int i, int n) { return (int)((int64_t)i * n / kRotDiv % n); }
 
@@ -131,7 +133,9 @@ __device__ inline void dma16(uint32_t lds, const void* sbase, uint32_t voff) {
 
 // Walk of the merged kv lists of the two q-blocks (2p, 2p + 1) of a pair,
 // skipping ids outside [0, n).  Each list is walked from its rotated start
-// (walk_target of q-block 2p, the same target for both), and the merge takes
+// (walk_target of q-block 2p, the same target for both; 0 for dense
+// attention, where every q-block of a unit lists the same blocks and the
+// natural order already keeps them together), and the merge takes
 // the smaller of the two heads in that rotated order, key (id - target) mod n,
 // so a block both lists hold is visited once.  All lanes hold the same state
 // (it lives in scalar registers).  KV2: the lists hold kv blocks of 128 tokens
@@ -149,7 +153,8 @@ struct PairWalk {
     n = a.n;
     dense = is_dense;
     const int ia = 2 * ip, ib = 2 * ip + 1;
-    target = walk_target(ia, n);
+    // without a mask every q-block lists every block: natural order from block 0
+    target = dense ? 0 : walk_target(ia, n);
     if (dense) {
       a0 = 0;
       la = n;

@@ -146,9 +146,10 @@ void attn_fwd_16_kernel(AttnArgs a) {
   }
   ConstI32* cidx = as_constant(a.col_idx);   // scalar loads
   auto kv_at = [&](int p) { return DENSE ? p : KV2 ? 2 * cidx[p >> 1] + (p & 1) : cidx[p]; };
-  // walk step v visits list position kb0 + (v + rot) mod L (see walk_target)
+  // walk step v visits list position kb0 + (v + rot) mod L (see walk_target);
+  // without a mask every q-block lists every block and starts at block 0
   const int L = kb1 - kb0;
-  const int rot = walk_rotation(kb0, kb1, walk_target(i, n), kv_at);
+  const int rot = DENSE ? 0 : walk_rotation(kb0, kb1, walk_target(i, n), kv_at);
   auto kv_block = [&](int v) {
     const int p = v + rot;
     return kv_at(kb0 + (p >= L ? p - L : p));
