@@ -48,14 +48,27 @@ __global__ __launch_bounds__(64) void pool_kernel(TensorArg q, TensorArg k, int 
   // for which the fma is the plain sum
   const int n_scaled = which ? ks.n_first : 0;
   const double beta = (double)ks.beta;
-  for (int tok = g; tok < cnt; tok += 4) {
-    const uint4 raw = *reinterpret_cast<const uint4*>(base + (int64_t)(t0 + tok) * t.ss);
-    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-    const double wt = t0 + tok < n_scaled ? beta : 1.0;
+  // 64 tokens at a time: the lane's 16 loads (tokens g, g + 4, ...) are all
+  // issued before the first is summed, so a wave keeps 16 KB in flight; the
+  // sums still run in token order
+  for (int c0 = 0; c0 < cnt; c0 += 64) {
+    uint4 raw[16];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc[2 * e] = __builtin_fma(wt, (double)to_f32(uint16_t(w[e] & 0xffff), bf16), acc[2 * e]);
-      acc[2 * e + 1] = __builtin_fma(wt, (double)to_f32(uint16_t(w[e] >> 16), bf16), acc[2 * e + 1]);
+    for (int u = 0; u < 16; ++u) {
+      const int tok = c0 + g + 4 * u;
+      raw[u] = tok < cnt ? *reinterpret_cast<const uint4*>(base + (int64_t)(t0 + tok) * t.ss) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int tok = c0 + g + 4 * u;
+      if (tok >= cnt) break;
+      const uint32_t w[4] = {raw[u].x, raw[u].y, raw[u].z, raw[u].w};
+      const double wt = t0 + tok < n_scaled ? beta : 1.0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] = __builtin_fma(wt, (double)to_f32(uint16_t(w[e] & 0xffff), bf16), acc[2 * e]);
+        acc[2 * e + 1] = __builtin_fma(wt, (double)to_f32(uint16_t(w[e] >> 16), bf16), acc[2 * e + 1]);
+      }
     }
   }
 #pragma unroll
@@ -96,20 +109,33 @@ __global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* 
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
   const int n_scaled = which ? ks.n_first : 0;
   const double beta = (double)ks.beta;
-  for (int tok = g; tok < cnt; tok += 4) {
-    const uint2 raw = *reinterpret_cast<const uint2*>(base + (int64_t)(t0 + tok) * t.ss);
-    // the token's value is code * (scale of its 64-token block)
-    const double wt = (t0 + tok < n_scaled ? beta : 1.0) * (double)sc[(t0 + tok) / kBlock];
-    // v_cvt_pk_f32_fp8 decodes OCP e4m3fn exactly: each of the 256 codes gives
-    // the value of its fields (bias 7, three mantissa bits, subnormals
-    // m * 2^-9, S.1111.111 NaN)
-    const auto f01 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw.x, false);
-    const auto f23 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw.x, true);
-    const auto f45 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw.y, false);
-    const auto f67 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw.y, true);
-    const float f[8] = {f01[0], f01[1], f23[0], f23[1], f45[0], f45[1], f67[0], f67[1]};
+  // 64 tokens at a time, all 16 loads of a lane issued before the sums (as in
+  // pool_kernel); the sums run in token order
+  for (int c0 = 0; c0 < cnt; c0 += 64) {
+    uint2 raw[16];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = __builtin_fma(wt, (double)f[e], acc[e]);
+    for (int u = 0; u < 16; ++u) {
+      const int tok = c0 + g + 4 * u;
+      raw[u] = tok < cnt ? *reinterpret_cast<const uint2*>(base + (int64_t)(t0 + tok) * t.ss) : make_uint2(0, 0);
+    }
+    // the tokens' values are code * (scale of their 64-token block)
+    const double sc_blk = (double)sc[(t0 + c0) / kBlock];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int tok = c0 + g + 4 * u;
+      if (tok >= cnt) break;
+      const double wt = (t0 + tok < n_scaled ? beta : 1.0) * sc_blk;
+      // v_cvt_pk_f32_fp8 decodes OCP e4m3fn exactly: each of the 256 codes
+      // gives the value of its fields (bias 7, three mantissa bits, subnormals
+      // m * 2^-9, S.1111.111 NaN)
+      const auto f01 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw[u].x, false);
+      const auto f23 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw[u].x, true);
+      const auto f45 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw[u].y, false);
+      const auto f67 = __builtin_amdgcn_cvt_pk_f32_fp8((int)raw[u].y, true);
+      const float f[8] = {f01[0], f01[1], f23[0], f23[1], f45[0], f45[1], f67[0], f67[1]};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = __builtin_fma(wt, (double)f[e], acc[e]);
+    }
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
