@@ -18,11 +18,14 @@ __device__ inline float to_f32(uint16_t bits, bool is_bf16) {
 }
 
 // One workgroup of 256 threads per (b, h, block); thread t owns tokens
-// t/16 + 16u (u = 0..3) and the 8-value column chunk (t % 16) * 8.
+// t/16 + 16u (u = 0..3) and the 8-value column chunk (t % 16) * 8.  The
+// grid runs the heads fastest, so the workgroups in flight together cover
+// whole token rows of the [B, S, H, D] tensor rather than one head's 256
+// bytes of many rows.
 __global__ __launch_bounds__(256) void quant_fp8_kernel(TensorArg x, TensorArg codes, int S, int H, int n,
                                                         bool bf16, float* __restrict__ scales) {
   __shared__ float red[4];
-  const int blk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int h = blockIdx.x, blk = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
   const int c = (tid & 15) * 8;
   const int t0 = blk * kBlock;
@@ -30,22 +33,22 @@ __global__ __launch_bounds__(256) void quant_fp8_kernel(TensorArg x, TensorArg c
   const uint16_t* src = static_cast<const uint16_t*>(x.data) + (int64_t)b * x.sb + (int64_t)h * x.sh + c;
   uint8_t* dst = static_cast<uint8_t*>(const_cast<void*>(codes.data)) + (int64_t)b * codes.sb +
                  (int64_t)h * codes.sh + c;
+  // all four loads of the thread are issued before the first is used
+  uint4 raw[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int tok = (tid >> 4) + 16 * u;
+    raw[u] = tok < cnt ? *reinterpret_cast<const uint4*>(src + (int64_t)(t0 + tok) * x.ss) : make_uint4(0, 0, 0, 0);
+  }
   float v[4][8];
   float amax = 0.f;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int tok = (tid >> 4) + 16 * u;
-    if (tok < cnt) {
-      const uint4 raw = *reinterpret_cast<const uint4*>(src + (int64_t)(t0 + tok) * x.ss);
-      const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+    const uint32_t w[4] = {raw[u].x, raw[u].y, raw[u].z, raw[u].w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        v[u][2 * e] = to_f32(uint16_t(w[e] & 0xffff), bf16);
-        v[u][2 * e + 1] = to_f32(uint16_t(w[e] >> 16), bf16);
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[u][e] = 0.f;
+    for (int e = 0; e < 4; ++e) {
+      v[u][2 * e] = to_f32(uint16_t(w[e] & 0xffff), bf16);
+      v[u][2 * e + 1] = to_f32(uint16_t(w[e] >> 16), bf16);
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(v[u][e]));
@@ -80,7 +83,7 @@ __global__ __launch_bounds__(256) void quant_fp8_kernel(TensorArg x, TensorArg c
 hipError_t launch_quant_fp8(chorus_dtype in_dt, TensorArg x, TensorArg codes, int B, int S, int H, float* scales,
                             hipStream_t st) {
   const int n = blocks_of(S);
-  hipLaunchKernelGGL(quant_fp8_kernel, dim3(n, H, B), dim3(256), 0, st, x, codes, S, H, n, in_dt == CHORUS_BF16,
+  hipLaunchKernelGGL(quant_fp8_kernel, dim3(H, n, B), dim3(256), 0, st, x, codes, S, H, n, in_dt == CHORUS_BF16,
                      scales);
   return hipGetLastError();
 }
