@@ -152,8 +152,9 @@ __global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* 
 // ---------------------------------------------------------------------------
 // 2a. Block scores s = sm_scale * qbar kbar^T per (request, head), n x nk
 // (q-blocks x kv blocks): a float64 GEMM on the matrix cores
-// (v_mfma_f64_16x16x4f64), one 128 x 128 output tile per workgroup of four
-// waves, each wave a 64 x 64 quarter as 4 x 4 MFMA tiles.  The head dim is
+// (v_mfma_f64_16x16x4f64), one 128 x 128 output tile per workgroup of eight
+// waves, each wave a 64 x 32 eighth as 4 x 2 MFMA tiles (112 registers, so a
+// SIMD holds four such waves: two workgroups per CU).  The head dim is
 // staged through LDS sixteen at a time (both operands k-major, so a lane's
 // fragment is one float64 of a row); the next chunk is fetched into
 // registers while the current one is multiplied.  Writes float64 scores
@@ -163,7 +164,7 @@ constexpr int kST = 128;  // score tile
 constexpr int kSK = 16;   // k-chunk
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void score_kernel(const double* __restrict__ qbar,
+__global__ __launch_bounds__(512) void score_kernel(const double* __restrict__ qbar,
                                                     const double* __restrict__ kbar, int n, int nk, double sm_scale,
                                                     double* __restrict__ scores, float* __restrict__ scores32) {
   __shared__ double qs[kSK][kST + 2];
@@ -174,65 +175,63 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void s
   const double* kb = kbar + (int64_t)bh * nk * kHeadDim;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave >> 2, wc = wave & 3;   // 64-row half, 32-column quarter
   const int li = lane & 15, lk = lane >> 4;
-  const bool wave_live = i0 + wr * 64 < n && j0 + wc * 64 < nk;
-  // staging: thread -> (row r, dims d0 .. d0 + 7) of each operand's chunk
-  const int sr = tid >> 1, sd0 = (tid & 1) * 8;
+  const bool wave_live = i0 + wr * 64 < n && j0 + wc * 32 < nk;
+  // staging: thread -> (row r, dims d0 .. d0 + 3) of each operand's chunk
+  const int sr = tid >> 2, sd0 = (tid & 3) * 4;
   const bool qin = i0 + sr < n, kin = j0 + sr < nk;
   const double* qrow = qb + (int64_t)(qin ? i0 + sr : 0) * kHeadDim + sd0;
   const double* krow = kb + (int64_t)(kin ? j0 + sr : 0) * kHeadDim + sd0;
-  double qv[8], kv[8];
+  double qv[4], kv[4];
 #pragma unroll
-  for (int d = 0; d < 8; ++d) {
+  for (int d = 0; d < 4; ++d) {
     qv[d] = qin ? qrow[d] : 0.0;
     kv[d] = kin ? krow[d] : 0.0;
   }
-  f64x4 acc[4][4];
+  f64x4 acc[4][2];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[a][c] = (f64x4){0.0, 0.0, 0.0, 0.0};
+    for (int c = 0; c < 2; ++c) acc[a][c] = (f64x4){0.0, 0.0, 0.0, 0.0};
   for (int kk = 0; kk < kHeadDim; kk += kSK) {
     __syncthreads();   // the previous chunk is no longer read
 #pragma unroll
-    for (int d = 0; d < 8; ++d) {
+    for (int d = 0; d < 4; ++d) {
       qs[sd0 + d][sr] = qv[d];
       ks[sd0 + d][sr] = kv[d];
     }
     __syncthreads();
     if (kk + kSK < kHeadDim) {
 #pragma unroll
-      for (int d = 0; d < 8; ++d) {
+      for (int d = 0; d < 4; ++d) {
         qv[d] = qin ? qrow[kk + kSK + d] : 0.0;
         kv[d] = kin ? krow[kk + kSK + d] : 0.0;
       }
     }
-    // a wave whose 64 rows or 64 columns all lie past the matrix edge only
+    // a wave whose 64 rows or 32 columns all lie past the matrix edge only
     // helps stage the operands.  A[i][k]: lane holds row i = li of the tile,
     // k = lk; B[k][j]: column j = li.  The fragments of the next k-step are
-    // read while this step's 16 products run.
+    // read while this step's 8 products run.
     if (wave_live) {
-      double af[2][4], bf[2][4];
+      double af[2][4], bf[2][2];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        af[0][t] = qs[lk][wr * 64 + t * 16 + li];
-        bf[0][t] = ks[lk][wc * 64 + t * 16 + li];
-      }
+      for (int t = 0; t < 4; ++t) af[0][t] = qs[lk][wr * 64 + t * 16 + li];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) bf[0][t] = ks[lk][wc * 32 + t * 16 + li];
 #pragma unroll
       for (int k4 = 0; k4 < kSK; k4 += 4) {
         const int cur = (k4 / 4) & 1;
         if (k4 + 4 < kSK) {
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            af[cur ^ 1][t] = qs[k4 + 4 + lk][wr * 64 + t * 16 + li];
-            bf[cur ^ 1][t] = ks[k4 + 4 + lk][wc * 64 + t * 16 + li];
-          }
+          for (int t = 0; t < 4; ++t) af[cur ^ 1][t] = qs[k4 + 4 + lk][wr * 64 + t * 16 + li];
+#pragma unroll
+          for (int t = 0; t < 2; ++t) bf[cur ^ 1][t] = ks[k4 + 4 + lk][wc * 32 + t * 16 + li];
         }
 #pragma unroll
         for (int a = 0; a < 4; ++a)
 #pragma unroll
-          for (int c = 0; c < 4; ++c)
+          for (int c = 0; c < 2; ++c)
             acc[a][c] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[cur][a], bf[cur][c], acc[a][c], 0, 0, 0);
       }
     }
@@ -240,13 +239,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void s
   // D tile element (4 r + lane / 16, lane % 16) sits in register r of the lane
   if (i0 + kST <= n && j0 + kST <= nk && !scores32) {
     // interior tile, float64 scores only: no per-element checks
-    double* out = scores + ((int64_t)bh * n + i0 + wr * 64 + lk) * nk + j0 + wc * 64 + li;
+    double* out = scores + ((int64_t)bh * n + i0 + wr * 64 + lk) * nk + j0 + wc * 32 + li;
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) out[(int64_t)(a * 16 + 4 * r) * nk + c * 16] = sm_scale * acc[a][c][r];
+        for (int c = 0; c < 2; ++c) out[(int64_t)(a * 16 + 4 * r) * nk + c * 16] = sm_scale * acc[a][c][r];
     return;
   }
 #pragma unroll
@@ -256,8 +255,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void s
       const int i = i0 + wr * 64 + a * 16 + 4 * r + lk;
       if (i >= n) continue;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int j = j0 + wc * 64 + c * 16 + li;
+      for (int c = 0; c < 2; ++c) {
+        const int j = j0 + wc * 32 + c * 16 + li;
         if (j >= nk) continue;
         const double v = sm_scale * acc[a][c][r];
         const int64_t o = ((int64_t)bh * n + i) * nk + j;
@@ -1292,7 +1291,7 @@ hipError_t launch_score_select(const double* qbar, const double* kbar, int B, in
                                double sm_scale, double top_p, int k_min, double* scores, int32_t* counts,
                                uint32_t* bitmap, int words, float* block_scores, hipStream_t st) {
   const int tiles_q = (n + kST - 1) / kST, tiles_k = (nk + kST - 1) / kST;
-  hipLaunchKernelGGL(score_kernel, dim3(tiles_k, tiles_q, B * H), dim3(256), 0, st, qbar, kbar, n, nk, sm_scale,
+  hipLaunchKernelGGL(score_kernel, dim3(tiles_k, tiles_q, B * H), dim3(512), 0, st, qbar, kbar, n, nk, sm_scale,
                      scores, block_scores);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
