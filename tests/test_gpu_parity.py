@@ -380,6 +380,53 @@ def test_attention_fp8_small_full():
         assert np.max(np.abs(lg[fin] - L[fin])) <= 1e-3
 
 
+@pytest.mark.parametrize("kind", ["bf16", "f16", "fp8"])
+def test_attention_skips_out_of_range_ids(kind):
+    """Ids outside [0, n) in a mask row are skipped (the contract in
+    include/chorus.h): rows with -1 ahead of their ids, or n and n + 5 after
+    them, give the output of the same rows without those ids, also where a
+    row holds nothing else.  Each q-block's kv walk starts at a rotated
+    position of its row, which has to land on the valid ids of such rows."""
+    gen = torch.Generator().manual_seed(5)
+    B, S, H = 1, 1000, 3
+    q, k, v = rand_qkv(gen, B, S, H, torch.float16 if kind == "f16" else torch.bfloat16)
+    n = (S + 63) // 64
+    rng = np.random.Generator(np.random.PCG64(11))
+    rp, ci = wk.random_csr(rng, H * n, n, 0.4, empty_frac=0.1)
+    rows = []
+    for r in range(H * n):
+        ids = [int(j) for j in ci[rp[r]:rp[r + 1]]]
+        if r % 3 == 0:
+            ids = [-1] + ids
+        elif r % 3 == 1:
+            ids = ids + [n, n + 5]
+        rows.append(ids)
+    assert any(len(x) == 1 and x[0] == -1 for x in rows)   # a row of invalid ids only
+    rp2 = np.concatenate([[0], np.cumsum([len(x) for x in rows])])
+    ci2 = np.array([j for x in rows for j in x], dtype=np.int64)
+    mask = ops.BlockMask.from_host(rp2, ci2, 1, H, n)
+    sm = 1.0 / math.sqrt(128)
+    if kind == "fp8":
+        (qc, qs), (kc, ks), (vc, vs) = (ops.quantize_fp8_blockwise(x.cuda()) for x in (q, k, v))
+        out, lse = ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs), sm_scale=sm,
+                                             return_lse=True)
+        deq = [of.dequantize_blockwise(c.cpu().numpy(), s_.cpu().numpy())
+               for c, s_ in ((qc, qs), (kc, ks), (vc, vs))]
+        O, L = oa.attention(*deq, rp, ci, sm, 1)
+        atol = TOL8
+    else:
+        out, lse = ops.block_sparse_attn_fwd(q.cuda(), k.cuda(), v.cuda(), mask, sm_scale=sm,
+                                             return_lse=True)
+        O, L = attn_ref_full(q, k, v, rp, ci, 1, sm)
+        atol = TOL16
+    torch.cuda.synchronize()
+    assert within_rounding(np64(out), O, torch.float16 if kind == "f16" else torch.bfloat16, atol=atol)
+    lg = lse.cpu().numpy()
+    fin = np.isfinite(L)
+    assert np.array_equal(np.isfinite(lg), fin)
+    assert np.max(np.abs(lg[fin] - L[fin])) <= 1e-3
+
+
 def test_attention_fp8_extreme_value_block_scales():
     """V blocks whose fp8 scale is zero-input (scale 1), denormal (values of
     order 1e-37) or large sit next to ordinary blocks in the same rows: the
