@@ -5,7 +5,10 @@
 A step is one pass of the whole hot path over one request batch with inputs
 resident in HBM: mask builder (block mean-pool, float64 block scores, top-p /
 top-k selection, CSR), work plan, [FP8 quantisation of Q, K, V for the fp8
-workload], and the block-sparse attention forward pass.  The metric is the
+workload], and the block-sparse attention forward pass.  When the fp8 path
+builds the mask from the request's own Q and K, the quantiser writes their
+float64 block sums as it reads them and the builder starts from those sums
+(the block mean-pool without a second pass over Q and K).  The metric is the
 effective TFLOP/s on computed blocks, 4 * 64 * 64 * 128 FLOP per computed
 (q-block, kv-block) pair, over the measured time.  Prints ONE JSON line.
 
@@ -396,23 +399,43 @@ def main():
     if fp8:
         codes = [torch.empty((B, S, H, 128), dtype=torch.uint8, device="cuda") for _ in range(3)]
         scales = [torch.empty((B, H, n), dtype=torch.float32, device="cuda") for _ in range(3)]
+    # a mask built from the request's own Q and K on the fp8 path takes the
+    # block sums that the quantiser writes while it reads Q and K, instead of
+    # a second pass over them
+    from_sums = fp8 and wl.mask_source == "self"
+    if from_sums:
+        sums = [torch.empty((B, H, n, 128), dtype=torch.float64, device="cuda") for _ in range(2)]
 
     kvb = args.kv_block
     if kvb != 64 and mq is None:
         sys.exit("--kv-block 128 needs a workload whose mask is built")
 
+    def build_from_qk():
+        return ops.build_block_mask(mq, mk, wl.top_p, wl.min_top_k, sm_scale=wl.sm_scale,
+                                    out=mask_buf, workspace=ws_build, kv_block=kvb)
+
     def build():
         if mq is None:
             return fixed
-        return ops.build_block_mask(mq, mk, wl.top_p, wl.min_top_k, sm_scale=wl.sm_scale,
-                                    out=mask_buf, workspace=ws_build, kv_block=kvb)
+        if from_sums:
+            return ops.build_block_mask_from_sums(sums[0], sums[1], S, wl.top_p, wl.min_top_k,
+                                                  sm_scale=wl.sm_scale, out=mask_buf, workspace=ws_build,
+                                                  kv_block=kvb)
+        return build_from_qk()
 
     def plan(m):
         return ops.plan_block_mask(m, B, S, out=order, workspace=ws_plan)
 
-    def quant():
+    def quant_plain():
         for x, c, s in zip((q, k, v), codes, scales):
             ops.quantize_fp8_blockwise(x, codes=c, scales=s)
+
+    def quant():
+        if not from_sums:
+            return quant_plain()
+        for x, c, s, t in zip((q, k), codes, scales, sums):
+            ops.quantize_fp8_blockwise_sums(x, codes=c, scales=s, block_sums=t)
+        ops.quantize_fp8_blockwise(v, codes=codes[2], scales=scales[2])
 
     def attn(m, sched, dense=False, key_scale=None):
         mm = None if dense else m
@@ -424,9 +447,11 @@ def main():
                                          schedule=sched, key_scale=key_scale)
 
     def step():
+        if from_sums:
+            quant()                   # codes, scales and the block sums of Q and K
         m = build()
         sched = plan(m)
-        if fp8:
+        if fp8 and not from_sums:
             quant()
         attn(m, sched)
 
@@ -512,6 +537,17 @@ def main():
     build_ms = event_ms(build, reps) if mq is not None else 0.0
     plan_ms = event_ms(lambda: plan(mask), reps)
     quant_ms = event_ms(quant, reps) if fp8 else 0.0
+    # with the mask from block sums, the routing cost is the builder from sums
+    # plus what the sums add to the quantiser; the builder that reads Q and K
+    # itself is timed beside it
+    build_qk_ms = quant_plain_ms = None
+    routing_ms = build_ms
+    if from_sums:
+        quant_plain_ms = event_ms(quant_plain, reps)
+        build_qk_ms = event_ms(build_from_qk, reps)
+        quant()
+        build()                       # the step's own mask again
+        routing_ms = build_ms + max(0.0, quant_ms - quant_plain_ms)
     build_fp8_ms = None
     if fp8 and mq is not None:
         # the builder reading fp8 codes of the mask source instead of 16-bit values
@@ -565,7 +601,9 @@ def main():
             "kv_block": kvb,
             "target_density": wl.density, "density": round(sub / float(mask.rows * n), 5),
             "top_p": wl.top_p, "min_top_k": wl.min_top_k, "computed_pairs": pairs,
-            "step": "mask build + plan" + (" + fp8 quantise" if fp8 else "") + " + attention",
+            "step": ("fp8 quantise (with Q, K block sums) + mask build from the sums + plan + attention"
+                     if from_sums else
+                     "mask build + plan" + (" + fp8 quantise" if fp8 else "") + " + attention"),
         },
         "attn_ms": round(attn_ms, 4),
         "attn_ms_per_launch": attn_stats,
@@ -573,19 +611,24 @@ def main():
         "attn_frac_mfma_peak": round(attn_tflops / peak, 4),
         "attn_key_scaled_ms": round(attn_ks_ms, 4),
         "builder_ms": round(build_ms, 4),
+        "builder_input": "block sums from the quantiser" if from_sums else ("Q, K" if mq is not None else None),
+        "builder_from_qk_ms": None if build_qk_ms is None else round(build_qk_ms, 4),
         "builder_fp8_input_ms": None if build_fp8_ms is None else round(build_fp8_ms, 4),
         "plan_ms": round(plan_ms, 4),
         "quant_ms": round(quant_ms, 4),
+        "quant_plain_ms": None if quant_plain_ms is None else round(quant_plain_ms, 4),
+        "routing_ms": round(routing_ms, 4),
         # HBM-bound stages: algorithmic bytes over time (the builder reads the
         # mask source's Q and K once; the quantiser reads 2 B and writes 1 B per
         # element of Q, K and V, plus the scales)
         "builder_gbps": (round(2 * mq.numel() * mq.element_size() / (build_ms * 1e-3) / 1e9, 1)
-                         if mq is not None and build_ms > 0 else None),
-        "quant_gbps": (round((3 * 3 * q.numel() + 3 * 4 * B * H * n) / (quant_ms * 1e-3) / 1e9, 1)
+                         if mq is not None and build_ms > 0 and not from_sums else None),
+        "quant_gbps": (round((3 * 3 * q.numel() + 3 * 4 * B * H * n + (16 * B * H * n * 128 if from_sums else 0))
+                             / (quant_ms * 1e-3) / 1e9, 1)
                        if fp8 and quant_ms > 0 else None),
         "visit_update_ms": round(visit_update_ms, 4),
         "visit_refresh_worst_ms": round(visit_refresh_ms, 4),
-        "routing_overhead_ratio": round(build_ms / (build_ms + attn_ms), 4),
+        "routing_overhead_ratio": round(routing_ms / (routing_ms + attn_ms), 4),
         "dense_attn_ms": round(dense_ms, 4),
         "speedup_vs_dense": round(dense_ms / attn_ms, 3),
         "ideal_speedup": round(float(mask.rows * n) / sub, 3),

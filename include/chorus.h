@@ -189,6 +189,23 @@ chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const choru
                                           float* block_scores, void* workspace,
                                           size_t workspace_bytes, void* stream);
 
+/* The builder from block sums (Sec. 3.2 Obs. 2, "Mask Caching and
+ * Retrieval"): q_sums and k_sums are the float64 [B, H, n_blocks, 128]
+ * 64-token block sums written by chorus_quantize_fp8_blockwise_sums for Q
+ * and K (any key scale already applied to k_sums).  Step 1 takes q_i = the
+ * sum of block i / its valid-token count and k_j = the sum of the 64-token
+ * blocks inside kv block j / its valid-token count; steps 2-7 and every
+ * other argument, check and output are those of chorus_build_block_mask
+ * (same workspace size).  The sums of 16-bit values over 64 or 128 tokens
+ * are exact in float64 for all but extreme exponent spreads, so the masks
+ * equal those of chorus_build_block_mask on the quantiser's input.  NULL
+ * q_sums or k_sums is CHORUS_ERR_INVALID_ARG. */
+chorus_status chorus_build_block_mask_from_sums(const chorus_shape* shape, const double* q_sums,
+                                                const double* k_sums, double sm_scale, double top_p,
+                                                double min_top_k, int32_t kv_block, int32_t* row_ptr,
+                                                int32_t* col_idx, int64_t col_capacity, float* block_scores,
+                                                void* workspace, size_t workspace_bytes, void* stream);
+
 /* The builder for callers that cannot allocate device memory (code under
  * HIP-graph capture, serving loops, harnesses that forbid hipMalloc): the
  * same arguments, checks and result as chorus_build_block_mask on f16 / bf16
@@ -268,6 +285,22 @@ chorus_status chorus_validate_block_mask(const chorus_block_mask* mask, int64_t 
 chorus_status chorus_quantize_fp8_blockwise(chorus_dtype in_dtype, const chorus_shape* shape,
                                             const chorus_tensor* x, const chorus_tensor* codes,
                                             float* scales, void* stream);
+
+/* The quantiser that also writes what step 1 of the mask builder needs
+ * (Sec. 3.2 Obs. 2: block means of Q and K), so that a step which quantises
+ * Q and K anyway does not read them a second time for the mask:
+ *   block_sums[b, h, i, d] = sum over the valid tokens c of 64-token block i
+ *                            of w_c * x[b, c, h, d], in float64,
+ * w_c = beta for c < n_first when key_scale is given (Eq. 1, for K), else 1.
+ * codes and scales are bitwise those of chorus_quantize_fp8_blockwise.
+ * block_sums : out, device float64 [B, H, n_blocks, 128], contiguous.
+ * key_scale  : optional (NULL for none); same checks as the builder's.
+ * Errors as chorus_quantize_fp8_blockwise; NULL block_sums is
+ * CHORUS_ERR_INVALID_ARG. */
+chorus_status chorus_quantize_fp8_blockwise_sums(chorus_dtype in_dtype, const chorus_shape* shape,
+                                                 const chorus_tensor* x, const chorus_tensor* codes,
+                                                 float* scales, const chorus_key_scale* key_scale,
+                                                 double* block_sums, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Block-sparse attention forward -- Sec. 3.2 "Efficient block-sparse kernel":

@@ -154,8 +154,35 @@ size_t chorus_build_block_mask_workspace_size(const chorus_shape* shape) {
   return bytes;
 }
 
-// Host checks shared by every builder entry point; on success fills the ids
-// per row (nk), the floor k_min and the key scale.
+// Host checks of the selection arguments and outputs, shared by every builder
+// entry point (shape already checked); on success fills the ids per row (nk)
+// and the floor k_min.
+static chorus_status check_selection(const chorus_shape* shape, double sm_scale, double top_p, double min_top_k,
+                                     int32_t kv_block, int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+                                     int* nk_out, int* k_min_out) {
+  const int n = blocks_of(shape->S);
+  if (n > kMaxBuilderBlocks)
+    return fail(CHORUS_ERR_UNSUPPORTED, "n_blocks=%d exceeds builder limit %d", n, kMaxBuilderBlocks);
+  if (!(top_p >= 0.0 && top_p <= 1.0)) return fail(CHORUS_ERR_INVALID_ARG, "top_p must be in [0, 1]");
+  if (!(min_top_k >= 0.0 && min_top_k <= 1.0))
+    return fail(CHORUS_ERR_INVALID_ARG, "min_top_k must be in [0, 1]");
+  if (!std::isfinite(sm_scale)) return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite");
+  if (!kv_block_ok(kv_block)) return fail(CHORUS_ERR_UNSUPPORTED, "kv_block %d unsupported (64 or 128)", kv_block);
+  if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
+  const int nk = (shape->S + kv_block - 1) / kv_block;
+  const int64_t rows = (int64_t)shape->B * shape->H * n;
+  if (rows * nk > INT32_MAX)
+    return fail(CHORUS_ERR_UNSUPPORTED, "rows*kv blocks = %lld exceeds int32 CSR offsets", (long long)(rows * nk));
+  if (col_capacity < rows * nk)
+    return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
+                (long long)(rows * nk));
+  *nk_out = nk;
+  *k_min_out = (int)std::ceil(min_top_k * (double)nk - 1e-9);
+  return CHORUS_OK;
+}
+
+// Host checks of the builder entry points that read Q and K; on success fills
+// nk, k_min and the key scale.
 static chorus_status check_build(chorus_dtype dtype, const chorus_shape* shape, const chorus_tensor* q,
                                  const float* q_scale, const chorus_tensor* k, const float* k_scale,
                                  double sm_scale, double top_p, double min_top_k, int32_t kv_block,
@@ -169,28 +196,27 @@ static chorus_status check_build(chorus_dtype dtype, const chorus_shape* shape, 
   if ((st = check_tensor(q, "q", fp8 ? 1 : 2))) return st;
   if ((st = check_tensor(k, "k", fp8 ? 1 : 2))) return st;
   if (fp8 && (!q_scale || !k_scale)) return fail(CHORUS_ERR_INVALID_ARG, "fp8 input needs q_scale and k_scale");
+  if ((st = check_selection(shape, sm_scale, top_p, min_top_k, kv_block, row_ptr, col_idx, col_capacity, nk_out,
+                            k_min_out)))
+    return st;
+  return check_key_scale(key_scale, shape->S, ks_out);
+}
+
+// Block scores, selection, CSR: steps 2-7 of the builder on the pooled means
+// already in the workspace.
+static chorus_status select_and_emit(const chorus_shape* shape, const BuilderWorkspace& w, int nk, double sm_scale,
+                                     double top_p, int k_min, int32_t* row_ptr, int32_t* col_idx,
+                                     float* block_scores, hipStream_t s) {
+  chorus_status st;
   const int n = blocks_of(shape->S);
-  if (n > kMaxBuilderBlocks)
-    return fail(CHORUS_ERR_UNSUPPORTED, "n_blocks=%d exceeds builder limit %d", n, kMaxBuilderBlocks);
-  if (!(top_p >= 0.0 && top_p <= 1.0)) return fail(CHORUS_ERR_INVALID_ARG, "top_p must be in [0, 1]");
-  if (!(min_top_k >= 0.0 && min_top_k <= 1.0))
-    return fail(CHORUS_ERR_INVALID_ARG, "min_top_k must be in [0, 1]");
-  if (!std::isfinite(sm_scale)) return fail(CHORUS_ERR_INVALID_ARG, "sm_scale must be finite");
-  if (!kv_block_ok(kv_block)) return fail(CHORUS_ERR_UNSUPPORTED, "kv_block %d unsupported (64 or 128)", kv_block);
-  KeyScale ks;
-  if ((st = check_key_scale(key_scale, shape->S, &ks))) return st;
-  if (!row_ptr || !col_idx) return fail(CHORUS_ERR_INVALID_ARG, "row_ptr/col_idx is NULL");
-  const int nk = (shape->S + kv_block - 1) / kv_block;
   const int64_t rows = (int64_t)shape->B * shape->H * n;
-  if (rows * nk > INT32_MAX)
-    return fail(CHORUS_ERR_UNSUPPORTED, "rows*kv blocks = %lld exceeds int32 CSR offsets", (long long)(rows * nk));
-  if (col_capacity < rows * nk)
-    return fail(CHORUS_ERR_CAPACITY, "col_capacity %lld < worst case %lld", (long long)col_capacity,
-                (long long)(rows * nk));
-  *nk_out = nk;
-  *k_min_out = (int)std::ceil(min_top_k * (double)nk - 1e-9);
-  *ks_out = ks;
-  return CHORUS_OK;
+  const int words = (nk + 31) / 32;
+  if ((st = from_hip(launch_score_select(w.qbar, w.kbar, shape->B, shape->H, n, nk, sm_scale, top_p, k_min,
+                                         w.scores, w.counts, w.bitmap, words, block_scores, s),
+                     "score_select")))
+    return st;
+  if ((st = from_hip(launch_scan_counts(w.counts, rows, row_ptr, s), "scan"))) return st;
+  return from_hip(launch_compact(w.bitmap, words, row_ptr, rows, col_idx, s), "compact");
 }
 
 static chorus_status build_mask_impl(chorus_dtype dtype, const chorus_shape* shape, const chorus_tensor* q,
@@ -208,23 +234,16 @@ static chorus_status build_mask_impl(chorus_dtype dtype, const chorus_shape* sha
     return st;
   const bool fp8 = dtype == CHORUS_FP8_E4M3;
   const int n = blocks_of(shape->S);
-  const int64_t rows = (int64_t)shape->B * shape->H * n;
   size_t need = 0;
   BuilderWorkspace w = carve_builder(workspace, shape->B, shape->H, n, &need);   // sized for nk <= n
   if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
-  const int words = (nk + 31) / 32;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const hipError_t pe = fp8 ? launch_pool_fp8(targ(q), q_scale, targ(k), k_scale, shape->B, shape->S, shape->H,
                                               kv_block, ks, w.qbar, w.kbar, s)
                             : launch_pool(dtype, targ(q), targ(k), shape->B, shape->S, shape->H, kv_block, ks,
                                           w.qbar, w.kbar, s);
   if ((st = from_hip(pe, "pool"))) return st;
-  if ((st = from_hip(launch_score_select(w.qbar, w.kbar, shape->B, shape->H, n, nk, sm_scale, top_p, k_min,
-                                         w.scores, w.counts, w.bitmap, words, block_scores, s),
-                     "score_select")))
-    return st;
-  if ((st = from_hip(launch_scan_counts(w.counts, rows, row_ptr, s), "scan"))) return st;
-  return from_hip(launch_compact(w.bitmap, words, row_ptr, rows, col_idx, s), "compact");
+  return select_and_emit(shape, w, nk, sm_scale, top_p, k_min, row_ptr, col_idx, block_scores, s);
 }
 
 chorus_status chorus_build_block_mask(chorus_dtype dtype, const chorus_shape* shape,
@@ -252,6 +271,30 @@ chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const choru
   return build_mask_impl(CHORUS_FP8_E4M3, shape, q, q_scale, k, k_scale, sm_scale, top_p, min_top_k, kv_block,
                          key_scale, row_ptr, col_idx, col_capacity, block_scores, workspace, workspace_bytes,
                          stream);
+}
+
+chorus_status chorus_build_block_mask_from_sums(const chorus_shape* shape, const double* q_sums,
+                                                const double* k_sums, double sm_scale, double top_p,
+                                                double min_top_k, int32_t kv_block, int32_t* row_ptr,
+                                                int32_t* col_idx, int64_t col_capacity, float* block_scores,
+                                                void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if (!q_sums || !k_sums) return fail(CHORUS_ERR_INVALID_ARG, "q_sums/k_sums is NULL");
+  int nk = 0, k_min = 0;
+  if ((st = check_selection(shape, sm_scale, top_p, min_top_k, kv_block, row_ptr, col_idx, col_capacity, &nk,
+                            &k_min)))
+    return st;
+  size_t need = 0;
+  BuilderWorkspace w = carve_builder(workspace, shape->B, shape->H, blocks_of(shape->S), &need);
+  if ((st = check_workspace(workspace, workspace_bytes, need))) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((st = from_hip(launch_means_from_sums(q_sums, k_sums, shape->B, shape->S, shape->H, kv_block, w.qbar, w.kbar,
+                                            s),
+                     "means")))
+    return st;
+  return select_and_emit(shape, w, nk, sm_scale, top_p, k_min, row_ptr, col_idx, block_scores, s);
 }
 
 chorus_status chorus_build_block_mask_noalloc(chorus_dtype dtype, const chorus_shape* shape,
@@ -327,8 +370,27 @@ chorus_status chorus_quantize_fp8_blockwise(chorus_dtype in_dtype, const chorus_
   if ((st = check_tensor(codes, "codes", 1))) return st;
   if (!scales) return fail(CHORUS_ERR_INVALID_ARG, "scales is NULL");
   return from_hip(launch_quant_fp8(in_dtype, targ(x), targ(codes), shape->B, shape->S, shape->H, scales,
-                                   static_cast<hipStream_t>(stream)),
+                                   KeyScale{0, 1.f}, nullptr, static_cast<hipStream_t>(stream)),
                   "quant_fp8");
+}
+
+chorus_status chorus_quantize_fp8_blockwise_sums(chorus_dtype in_dtype, const chorus_shape* shape,
+                                                 const chorus_tensor* x, const chorus_tensor* codes,
+                                                 float* scales, const chorus_key_scale* key_scale,
+                                                 double* block_sums, void* stream) {
+  g_last_error[0] = 0;
+  chorus_status st;
+  if ((st = check_shape(shape))) return st;
+  if (in_dtype != CHORUS_F16 && in_dtype != CHORUS_BF16)
+    return fail(CHORUS_ERR_UNSUPPORTED, "quantiser input dtype %d unsupported (f16/bf16)", (int)in_dtype);
+  if ((st = check_tensor(x, "x", 2))) return st;
+  if ((st = check_tensor(codes, "codes", 1))) return st;
+  if (!scales || !block_sums) return fail(CHORUS_ERR_INVALID_ARG, "scales/block_sums is NULL");
+  KeyScale ks;
+  if ((st = check_key_scale(key_scale, shape->S, &ks))) return st;
+  return from_hip(launch_quant_fp8(in_dtype, targ(x), targ(codes), shape->B, shape->S, shape->H, scales, ks,
+                                   block_sums, static_cast<hipStream_t>(stream)),
+                  "quant_fp8_sums");
 }
 
 size_t chorus_attn_workspace_size(chorus_dtype dtype, const chorus_shape* shape, const chorus_block_mask* mask) {

@@ -63,6 +63,9 @@ hipError_t launch_pool(chorus_dtype dt, TensorArg q, TensorArg k, int B, int S, 
                        double* qbar, double* kbar, hipStream_t st);
 hipError_t launch_pool_fp8(TensorArg q, const float* q_scale, TensorArg k, const float* k_scale, int B, int S,
                            int H, int kvb, KeyScale ks, double* qbar, double* kbar, hipStream_t st);
+// block means from the fp8 quantiser's 64-token column sums [B, H, n, 128]
+hipError_t launch_means_from_sums(const double* q_sums, const double* k_sums, int B, int S, int H, int kvb,
+                                  double* qbar, double* kbar, hipStream_t st);
 hipError_t launch_score_select(const double* qbar, const double* kbar, int B, int H, int n, int nk,
                                double sm_scale, double top_p, int k_min, double* scores,
                                int32_t* counts, uint32_t* bitmap, int words, float* block_scores,
@@ -98,8 +101,10 @@ hipError_t launch_visit_refresh(const int32_t* row_ptr, const int32_t* col_idx, 
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t count, hipStream_t st);
 
 // ---- fp8 quantiser (quant_fp8.hip) ----
+// sums == nullptr: codes and scales only; otherwise also the float64 block
+// column sums [B, H, n, 128] (first-frame tokens weighted by ks.beta)
 hipError_t launch_quant_fp8(chorus_dtype in_dt, TensorArg x, TensorArg codes, int B, int S, int H,
-                            float* scales, hipStream_t st);
+                            float* scales, KeyScale ks, double* sums, hipStream_t st);
 
 // ---- attention (attn_fwd.hip, attn_fwd_fp8.hip) ----
 struct AttnArgs {

@@ -149,6 +149,29 @@ __global__ __launch_bounds__(64) void pool_fp8_kernel(TensorArg q, const float* 
   }
 }
 
+// 1c. Block means from the column sums that the fp8 quantiser writes per
+// 64-token block (same weights as pool_kernel): a kv block of 128 tokens
+// adds the sums of its two halves.  One thread per (tensor, request, head,
+// block, column).
+__global__ __launch_bounds__(kHeadDim) void means_from_sums_kernel(const double* __restrict__ q_sums,
+                                                                   const double* __restrict__ k_sums, int S, int H,
+                                                                   int n, int kvb, int nk, double* __restrict__ qbar,
+                                                                   double* __restrict__ kbar) {
+  const int blk = blockIdx.x, h = blockIdx.y;
+  const int b = blockIdx.z >> 1, which = blockIdx.z & 1;
+  const int bs = which ? kvb : kBlock;
+  const int nb = which ? nk : n;
+  if (blk >= nb) return;
+  const int d = threadIdx.x;
+  const double* src = (which ? k_sums : q_sums) + (int64_t)(b * H + h) * n * kHeadDim + d;
+  const int t0 = blk * bs;
+  const int cnt = min(bs, S - t0);
+  const int s1 = (t0 + cnt + kBlock - 1) / kBlock;   // 64-token blocks t0 / 64 .. s1 - 1
+  double acc = 0.0;
+  for (int s = t0 / kBlock; s < s1; ++s) acc += src[(int64_t)s * kHeadDim];
+  (which ? kbar : qbar)[((int64_t)(b * H + h) * nb + blk) * kHeadDim + d] = acc / (double)cnt;
+}
+
 // ---------------------------------------------------------------------------
 // 2a. Block scores s = sm_scale * qbar kbar^T per (request, head), n x nk
 // (q-blocks x kv blocks): a float64 GEMM on the matrix cores
@@ -1247,6 +1270,14 @@ hipError_t launch_pool_fp8(TensorArg q, const float* q_scale, TensorArg k, const
   const int n = blocks_of(S), nk = (S + kvb - 1) / kvb;
   hipLaunchKernelGGL(pool_fp8_kernel, dim3(n, H, 2 * B), dim3(64), 0, st, q, q_scale, k, k_scale, S, H, n, kvb, nk,
                      ks, qbar, kbar);
+  return hipGetLastError();
+}
+
+hipError_t launch_means_from_sums(const double* q_sums, const double* k_sums, int B, int S, int H, int kvb,
+                                  double* qbar, double* kbar, hipStream_t st) {
+  const int n = blocks_of(S), nk = (S + kvb - 1) / kvb;
+  hipLaunchKernelGGL(means_from_sums_kernel, dim3(n, H, 2 * B), dim3(kHeadDim), 0, st, q_sums, k_sums, S, H, n, kvb,
+                     nk, qbar, kbar);
   return hipGetLastError();
 }
 

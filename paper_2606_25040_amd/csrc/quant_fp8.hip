@@ -7,6 +7,10 @@
 //   reciprocal, which would overflow below 448 / FLT_MAX; the codes depend on
 //   x / amax only, so every other block is unchanged.
 // HBM-bound: each value is read once (2 bytes) and written once (1 byte).
+// The SUMS variant also writes, per block, the float64 sum over its valid
+// tokens of each of the 128 columns (first-frame tokens weighted by beta when
+// a key scale is given, Eq. 1): the mask builder's block means (Sec. 3.2
+// Obs. 2) then need no second pass over Q and K.
 #include "chorus_internal.h"
 
 namespace chorus {
@@ -22,9 +26,12 @@ __device__ inline float to_f32(uint16_t bits, bool is_bf16) {
 // grid runs the heads fastest, so the workgroups in flight together cover
 // whole token rows of the [B, S, H, D] tensor rather than one head's 256
 // bytes of many rows.
+template <bool SUMS>
 __global__ __launch_bounds__(256) void quant_fp8_kernel(TensorArg x, TensorArg codes, int S, int H, int n,
-                                                        bool bf16, float* __restrict__ scales) {
+                                                        bool bf16, float* __restrict__ scales, KeyScale ks,
+                                                        double* __restrict__ sums) {
   __shared__ float red[4];
+  __shared__ double part[SUMS ? 4 * kHeadDim : 1];   // per-wave column sums
   const int h = blockIdx.x, blk = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
   const int c = (tid & 15) * 8;
@@ -53,10 +60,36 @@ __global__ __launch_bounds__(256) void quant_fp8_kernel(TensorArg x, TensorArg c
 #pragma unroll
     for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(v[u][e]));
   }
+  if (SUMS) {
+    // column sums of the thread's four tokens (rows past the block end hold
+    // zeros), then over the four token rows of the wave (lanes l ^ 16, l ^ 32)
+    double acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+    const double beta = (double)ks.beta;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const double wt = t0 + (tid >> 4) + 16 * u < ks.n_first ? beta : 1.0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = __builtin_fma(wt, (double)v[u][e], acc[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc[e] += __shfl_xor(acc[e], 16);
+      acc[e] += __shfl_xor(acc[e], 32);
+    }
+    if ((tid & 63) < 16) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part[(tid >> 6) * kHeadDim + c + e] = acc[e];
+    }
+  }
   for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o));
   if ((tid & 63) == 0) red[tid >> 6] = amax;
   __syncthreads();
   amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  if (SUMS && tid < kHeadDim)
+    sums[(((int64_t)b * H + h) * n + blk) * kHeadDim + tid] =
+        (part[tid] + part[kHeadDim + tid]) + (part[2 * kHeadDim + tid] + part[3 * kHeadDim + tid]);
   const float up = amax < 0x1p-64f ? 0x1p64f : 1.f;
   const float inv = amax > 0.f ? 448.f / (amax * up) : 0.f;
   if (tid == 0) scales[((int64_t)b * H + h) * n + blk] = amax > 0.f ? amax / 448.f : 1.f;
@@ -81,10 +114,14 @@ __global__ __launch_bounds__(256) void quant_fp8_kernel(TensorArg x, TensorArg c
 }  // namespace
 
 hipError_t launch_quant_fp8(chorus_dtype in_dt, TensorArg x, TensorArg codes, int B, int S, int H, float* scales,
-                            hipStream_t st) {
+                            KeyScale ks, double* sums, hipStream_t st) {
   const int n = blocks_of(S);
-  hipLaunchKernelGGL(quant_fp8_kernel, dim3(H, n, B), dim3(256), 0, st, x, codes, S, H, n, in_dt == CHORUS_BF16,
-                     scales);
+  if (sums)
+    hipLaunchKernelGGL(quant_fp8_kernel<true>, dim3(H, n, B), dim3(256), 0, st, x, codes, S, H, n,
+                       in_dt == CHORUS_BF16, scales, ks, sums);
+  else
+    hipLaunchKernelGGL(quant_fp8_kernel<false>, dim3(H, n, B), dim3(256), 0, st, x, codes, S, H, n,
+                       in_dt == CHORUS_BF16, scales, ks, sums);
   return hipGetLastError();
 }
 

@@ -60,9 +60,9 @@ def _key_scale(key_scale):
 
 EXPORTS = [
     "chorus_build_block_mask_workspace_size", "chorus_build_block_mask", "chorus_build_block_mask_fp8",
-    "chorus_build_block_mask_noalloc",
+    "chorus_build_block_mask_noalloc", "chorus_build_block_mask_from_sums",
     "chorus_plan_workspace_size", "chorus_plan_block_mask", "chorus_validate_block_mask",
-    "chorus_quantize_fp8_blockwise", "chorus_attn_workspace_size",
+    "chorus_quantize_fp8_blockwise", "chorus_quantize_fp8_blockwise_sums", "chorus_attn_workspace_size",
     "chorus_block_sparse_attn_fwd", "chorus_block_sparse_attn_fwd_f16",
     "chorus_block_sparse_attn_fwd_bf16", "chorus_block_sparse_attn_fwd_fp8",
     "chorus_attn_block_mass", "chorus_select_block_mask_workspace_size", "chorus_select_block_mask",
@@ -94,10 +94,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                               P(KeyScale), VP, VP, I64, VP, VP, SZ, VP]),
         "chorus_build_block_mask_noalloc": (I32, [I32, P(Shape), P(Tensor), P(Tensor), F64, F64, F64, I32,
                                                   P(KeyScale), VP, VP, I64, VP, VP]),
+        "chorus_build_block_mask_from_sums": (I32, [P(Shape), VP, VP, F64, F64, F64, I32, VP, VP, I64, VP,
+                                                    VP, SZ, VP]),
         "chorus_plan_workspace_size": (SZ, [P(Shape), P(Mask)]),
         "chorus_plan_block_mask": (I32, [P(Shape), P(Mask), VP, VP, SZ, VP]),
         "chorus_validate_block_mask": (I32, [P(Mask), I64, VP, VP]),
         "chorus_quantize_fp8_blockwise": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, VP]),
+        "chorus_quantize_fp8_blockwise_sums": (I32, [I32, P(Shape), P(Tensor), P(Tensor), VP, P(KeyScale), VP,
+                                                     VP]),
         "chorus_attn_workspace_size": (SZ, [I32, P(Shape), P(Mask)]),
         "chorus_block_sparse_attn_fwd": (I32, [I32, P(Shape), P(Tensor), P(Tensor), P(Tensor), VP,
                                                VP, VP, P(Mask), P(Schedule), F32, P(KeyScale),
@@ -345,6 +349,69 @@ def quantize_fp8_blockwise(x: torch.Tensor, codes: torch.Tensor | None = None,
                                          scales.data_ptr(), _stream())
     _check(st, "chorus_quantize_fp8_blockwise")
     return codes, scales
+
+
+def quantize_fp8_blockwise_sums(x: torch.Tensor, codes: torch.Tensor | None = None,
+                                scales: torch.Tensor | None = None, block_sums: torch.Tensor | None = None,
+                                key_scale=None):
+    """chorus_quantize_fp8_blockwise_sums: returns (codes, scales, block_sums float64 [B, H, n, 128]),
+    the sums over each 64-token block's valid tokens (first-frame tokens times
+    beta when ``key_scale = (n_first, beta)``)."""
+    L = load_library()
+    B, S, H, D = x.shape
+    n = (S + BLOCK - 1) // BLOCK
+    if codes is None:
+        codes = torch.empty((B, S, H, D), dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty((B, H, n), dtype=torch.float32, device=x.device)
+    if block_sums is None:
+        block_sums = torch.empty((B, H, n, D), dtype=torch.float64, device=x.device)
+    elif block_sums.shape != (B, H, n, D) or block_sums.dtype != torch.float64 or not block_sums.is_contiguous():
+        raise ValueError(f"block_sums must be a contiguous float64 [{B}, {H}, {n}, {D}] tensor")
+    st = L.chorus_quantize_fp8_blockwise_sums(_dtype_code(x), ctypes.byref(_shape(x)),
+                                              ctypes.byref(_tensor(x)), ctypes.byref(_tensor(codes)),
+                                              scales.data_ptr(), _key_scale(key_scale),
+                                              block_sums.data_ptr(), _stream())
+    _check(st, "chorus_quantize_fp8_blockwise_sums")
+    return codes, scales, block_sums
+
+
+def build_block_mask_from_sums(q_sums: torch.Tensor, k_sums: torch.Tensor, S: int, top_p: float,
+                               min_top_k: float, sm_scale: float | None = None, return_scores: bool = False,
+                               out: BlockMask | None = None, workspace: torch.Tensor | None = None,
+                               kv_block: int = BLOCK) -> BlockMask:
+    """chorus_build_block_mask_from_sums: the mask of sequence length ``S``
+    from the quantiser's float64 block sums ``[B, H, n, 128]`` of Q and K."""
+    L = load_library()
+    if q_sums.shape != k_sums.shape or q_sums.dim() != 4:
+        raise ValueError("q_sums and k_sums must share one [B, H, n, D] shape")
+    for t in (q_sums, k_sums):
+        if t.dtype != torch.float64 or not t.is_contiguous():
+            raise ValueError("block sums must be contiguous float64")
+    B, H, n, D = q_sums.shape
+    if n != (S + BLOCK - 1) // BLOCK:
+        raise ValueError(f"block sums hold {n} blocks, S = {S} needs {(S + BLOCK - 1) // BLOCK}")
+    nk = (S + kv_block - 1) // kv_block
+    rows = B * H * n
+    shape = Shape(B, S, H, D)
+    sm = 1.0 / math.sqrt(D) if sm_scale is None else float(sm_scale)
+    dev = q_sums.device
+    if out is None:
+        out = BlockMask(torch.empty(rows + 1, dtype=torch.int32, device=dev),
+                        torch.empty(rows * nk, dtype=torch.int32, device=dev), B, H, n, kv_block)
+    out.block = kv_block
+    if return_scores and (out.block_scores is None or out.block_scores.shape != (rows, nk)):
+        out.block_scores = torch.empty((rows, nk), dtype=torch.float32, device=dev)
+    need = L.chorus_build_block_mask_workspace_size(ctypes.byref(shape))
+    if workspace is None or workspace.numel() < need + 256:
+        workspace = _workspace(need, dev)
+    st = L.chorus_build_block_mask_from_sums(ctypes.byref(shape), q_sums.data_ptr(), k_sums.data_ptr(), sm,
+                                             float(top_p), float(min_top_k), int(kv_block), out.row_ptr.data_ptr(),
+                                             out.col_idx.data_ptr(), out.col_idx.numel(),
+                                             _ptr(out.block_scores if return_scores else None),
+                                             _aligned(workspace), need, _stream())
+    _check(st, "chorus_build_block_mask_from_sums")
+    return out
 
 
 def block_sparse_attn_fwd(q, k, v, mask: BlockMask | None, sm_scale: float | None = None,

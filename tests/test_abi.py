@@ -141,6 +141,38 @@ def test_other_entry_points_check_arguments(lib):
     assert lib.chorus_build_block_mask_workspace_size(ctypes.byref(shape(S=75600, H=40))) > 0
 
 
+def test_block_sums_entry_points_check_arguments(lib):
+    """The quantiser with block sums and the builder from sums reject bad
+    arguments on the host, before any device work."""
+    shp = shape()
+    t = t4()
+    ks_bad = ops.KeyScale(101, 1.5)                  # n_first > S
+    q = lib.chorus_quantize_fp8_blockwise_sums
+    assert q(ops.FP8_E4M3, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), FAKE, None, FAKE, None) == 2
+    assert q(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), FAKE, None, None, None) == 1
+    assert q(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), None, None, FAKE, None) == 1
+    assert q(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), FAKE, ctypes.byref(ks_bad), FAKE,
+             None) == 1
+    assert q(ops.BF16, ctypes.byref(shape(D=64)), ctypes.byref(t), ctypes.byref(t), FAKE, None, FAKE, None) == 2
+    b = lib.chorus_build_block_mask_from_sums
+    n = 2
+    need = lib.chorus_build_block_mask_workspace_size(ctypes.byref(shp))
+    cap = 2 * n * n
+
+    def call(qs=FAKE, kss=FAKE, top_p=0.5, mk=0.1, kvb=64, rp=FAKE, ci=FAKE, c=cap, ws=FAKE, wsb=need, sm=0.088):
+        return b(ctypes.byref(shp), qs, kss, sm, top_p, mk, kvb, rp, ci, c, None, ws, wsb, None)
+
+    assert call(qs=None) == 1
+    assert call(kss=None) == 1
+    assert call(top_p=1.5) == 1
+    assert call(mk=-0.1) == 1
+    assert call(kvb=96) == 2
+    assert call(rp=None) == 1
+    assert call(c=cap - 1) == 3
+    assert call(sm=float("inf")) == 1
+    assert call(wsb=need - 1) == 5
+
+
 def test_block_mass_selection_and_coverage_check_arguments(lib):
     shp = shape(B=1, S=100, H=2)
     t = t4()

@@ -1,0 +1,139 @@
+"""GPU parity of the fp8 quantiser with block sums and of the mask builder
+from block sums, through the C ABI: codes and scales bitwise those of the
+plain quantiser, the block means (Sec. 3.2 Obs. 2, step 1) equal to the
+oracle's, and the masks equal to the oracle's (comparator rule) and bitwise
+to those of the builder that reads Q and K itself, including kv blocks of
+128 tokens, ragged tails, the first-frame key enhancement (Eq. 1) and the
+720p 14B shape at full size."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import guidance as og
+from oracle import mask as om
+from paper_2606_25040_amd import ops
+import workloads as wk
+from tests.compare import compare_masks
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def device():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    ops.load_library()
+    torch.cuda.set_device(0)
+    yield
+
+
+def np64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def rand_x(seed, B, S, H, dtype, scale=0.5):
+    gen = torch.Generator().manual_seed(seed)
+    return (torch.randn(B, S, H, 128, generator=gen) * scale).to(dtype)
+
+
+def positional(B, S, H, dtype, seed):
+    """Q and K sharing a few sinusoidal directions, so that block scores have
+    structure and the selection keeps a few blocks per row."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    f = np.stack([np.sin(2 * np.pi * np.arange(S) / P) for P in (37.0, 200.0, 911.0)] +
+                 [np.cos(2 * np.pi * np.arange(S) / P) for P in (37.0, 200.0, 911.0)], 1)
+    q = np.empty((B, S, H, 128), np.float32)
+    k = np.empty((B, S, H, 128), np.float32)
+    for h in range(H):
+        W = g.standard_normal((6, 128)) * 0.5
+        for b in range(B):
+            q[b, :, h] = f @ W + 0.5 * g.standard_normal((S, 128))
+            k[b, :, h] = f @ W + 0.5 * g.standard_normal((S, 128))
+    return torch.from_numpy(q).to(dtype), torch.from_numpy(k).to(dtype)
+
+
+def counts(S, block=64):
+    n = (S + block - 1) // block
+    return np.array([min(block, S - i * block) for i in range(n)], dtype=np.float64)
+
+
+# betas exactly representable in fp32, so that the library's fp32 beta and the
+# oracle's float64 one scale the keys identically
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
+@pytest.mark.parametrize("S,key_scale", [(1000, None), (64, None), (130, (100, 1.5)), (1000, (640, 0.625)),
+                                         (2047, (2047, 2.0))])
+def test_quantizer_block_sums(dtype, S, key_scale):
+    """Codes and scales are bitwise the plain quantiser's; sums / valid count
+    equal the oracle's block means of the (enhanced) input exactly: a sum of
+    64 16-bit values (times an fp32 beta) is exact in float64 here."""
+    B, H = 2, 3
+    x = rand_x(S + 7, B, S, H, dtype).cuda()
+    codes, scales = ops.quantize_fp8_blockwise(x)
+    c2, s2, sums = ops.quantize_fp8_blockwise_sums(x, key_scale=key_scale)
+    torch.cuda.synchronize()
+    assert torch.equal(codes, c2)
+    assert torch.equal(scales.view(torch.int32), s2.view(torch.int32))
+    xs = np64(x)
+    if key_scale is not None:
+        xs = og.enhance_first_frame_keys(xs, *key_scale)
+    means = sums.cpu().numpy() / counts(S)[None, None, :, None]
+    for b in range(B):
+        for h in range(H):
+            ref = om.pool_means(xs[b, :, h])
+            assert np.array_equal(means[b, h], ref), float(np.max(np.abs(means[b, h] - ref)))
+
+
+@pytest.mark.parametrize("S,kv_block,top_p,mk,key_scale", [
+    (2000, 64, 0.6, 0.05, None),
+    (2000, 128, 0.6, 0.05, None),
+    (1090, 128, 0.9, 0.0, (300, 1.75)),
+    (960, 64, 0.0, 0.3, (600, 1.5)),
+    (4100, 64, 0.5, 0.0, (130, 0.75)),
+    (100, 64, 0.7, 0.1, None),
+])
+def test_mask_from_block_sums(S, kv_block, top_p, mk, key_scale):
+    """The mask from the quantiser's sums matches the oracle (every row exact
+    or a tie the comparator excuses) and is bitwise the mask, and the fp32
+    block scores, of the builder reading the same bf16 Q and K."""
+    B, H = 2, 2
+    q, k = positional(B, S, H, torch.bfloat16, S + kv_block)
+    q, k = q.cuda(), k.cuda()
+    sm = 1.0 / math.sqrt(128)
+    _, _, qs = ops.quantize_fp8_blockwise_sums(q)
+    _, _, kss = ops.quantize_fp8_blockwise_sums(k, key_scale=key_scale)
+    m = ops.build_block_mask_from_sums(qs, kss, S, top_p, mk, sm_scale=sm, return_scores=True,
+                                       kv_block=kv_block)
+    ref = ops.build_block_mask(q, k, top_p, mk, sm_scale=sm, return_scores=True, key_scale=key_scale,
+                               kv_block=kv_block)
+    torch.cuda.synchronize()
+    rp, ci = m.to_host()
+    rrp, rci = ref.to_host()
+    assert np.array_equal(rp, rrp) and np.array_equal(ci, rci)
+    assert torch.equal(m.block_scores.view(torch.int32), ref.block_scores.view(torch.int32))
+    ke = np64(k) if key_scale is None else og.enhance_first_frame_keys(np64(k), *key_scale)
+    o = om.build_block_mask(np64(q), ke, sm, top_p, mk, kv_block=kv_block)
+    rep = compare_masks(rp, ci, o, range(m.rows), top_p, mk)
+    assert rep.ok and not rep.failing, rep.failing[:3]
+
+
+def test_block_sums_full_size_720p_14b():
+    """At the 720p 14B shape (S = 75,600, H = 40, 1,182 blocks, a 48-token
+    tail block): the mask from block sums is bitwise the builder's on the same
+    Q and K, at the workload's top_p and floor, for kv blocks of 64 and 128."""
+    wl = wk.WORKLOADS["wan14b_720p_fp8"]
+    inp = wk.make_inputs(wl, with_v=False)
+    q, k = inp.mask_q.cuda(), inp.mask_k.cuda()
+    B, S, H, _ = q.shape
+    assert (S, H) == (75600, 40)
+    _, _, qs = ops.quantize_fp8_blockwise_sums(q)
+    _, _, kss = ops.quantize_fp8_blockwise_sums(k)
+    for kvb in (64, 128):
+        m = ops.build_block_mask_from_sums(qs, kss, S, wl.top_p, wl.min_top_k, sm_scale=wl.sm_scale,
+                                           kv_block=kvb)
+        ref = ops.build_block_mask(q, k, wl.top_p, wl.min_top_k, sm_scale=wl.sm_scale, kv_block=kvb)
+        torch.cuda.synchronize()
+        assert m.nnz == ref.nnz
+        assert torch.equal(m.row_ptr, ref.row_ptr)
+        assert torch.equal(m.col_idx[:m.nnz], ref.col_idx[:ref.nnz])

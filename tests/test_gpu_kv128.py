@@ -153,6 +153,51 @@ def test_attention_fp8_kv128(S):
     assert torch.equal(out.view(torch.int16), out64.view(torch.int16))
 
 
+@pytest.mark.parametrize("kind", ["bf16", "fp8"])
+def test_attention_kv128_skips_out_of_range_ids(kind):
+    """Ids of 128-token blocks outside [0, nk) are skipped: -1 ahead of a
+    row's ids, or nk and nk + 5 after them, leave the output of the clean
+    rows; both 64-token halves of such an id fall outside [0, n) and the
+    rotated walk start has to land on the valid halves."""
+    B, S, H = 1, 1090, 3
+    q, k, v = rand_qkv(19, B, S, H, torch.bfloat16)
+    n, nk = (S + 63) // 64, (S + 127) // 128
+    rng = np.random.Generator(np.random.PCG64(23))
+    rp, ci = wk.random_csr(rng, H * n, nk, 0.4, empty_frac=0.1)
+    rows = []
+    for r in range(H * n):
+        ids = [int(j) for j in ci[rp[r]:rp[r + 1]]]
+        if r % 3 == 0:
+            ids = [-1] + ids
+        elif r % 3 == 1:
+            ids = ids + [nk, nk + 5]
+        rows.append(ids)
+    assert any(len(x) == 1 and x[0] == -1 for x in rows)
+    rp2 = np.concatenate([[0], np.cumsum([len(x) for x in rows])])
+    ci2 = np.array([j for x in rows for j in x], dtype=np.int64)
+    mask = ops.BlockMask.from_host(rp2, ci2, 1, H, n, block=128)
+    sm = 1.0 / math.sqrt(128)
+    if kind == "fp8":
+        (qc, qs), (kc, ks), (vc, vs) = (ops.quantize_fp8_blockwise(x.cuda()) for x in (q, k, v))
+        out, lse = ops.block_sparse_attn_fwd(qc, kc, vc, mask, scales=(qs, ks, vs), sm_scale=sm,
+                                             return_lse=True)
+        deq = [of.dequantize_blockwise(c.cpu().numpy(), s_.cpu().numpy())
+               for c, s_ in ((qc, qs), (kc, ks), (vc, vs))]
+        O, L = oa.attention(*deq, rp, ci, sm, 1, kv_block=128)
+        atol = TOL8
+    else:
+        out, lse = ops.block_sparse_attn_fwd(q.cuda(), k.cuda(), v.cuda(), mask, sm_scale=sm,
+                                             return_lse=True)
+        O, L = oa.attention(np64(q), np64(k), np64(v), rp, ci, sm, 1, kv_block=128)
+        atol = TOL16
+    torch.cuda.synchronize()
+    assert within(np64(out), O, torch.bfloat16, atol), float(np.max(np.abs(np64(out) - O)))
+    lg = lse.cpu().numpy()
+    fin = np.isfinite(L)
+    assert np.array_equal(np.isfinite(lg), fin)
+    assert np.max(np.abs(lg[fin] - L[fin])) <= 1e-3
+
+
 @pytest.mark.parametrize("S,top_p,mk,key_scale", [(2000, 0.6, 0.05, None), (1090, 0.9, 0.0, None),
                                                   (960, 0.0, 0.3, (300, 1.7)), (64 * 4096, 0.5, 0.0, None)])
 def test_builder_kv128_matches_oracle(S, top_p, mk, key_scale):
