@@ -198,8 +198,8 @@ chorus_status chorus_build_block_mask_fp8(const chorus_shape* shape, const choru
  * other argument, check and output are those of chorus_build_block_mask
  * (same workspace size).  The sums of 16-bit values over 64 or 128 tokens
  * are exact in float64 for all but extreme exponent spreads, so the masks
- * equal those of chorus_build_block_mask on the quantiser's input.  NULL
- * q_sums or k_sums is CHORUS_ERR_INVALID_ARG. */
+ * equal those of chorus_build_block_mask on the quantiser's input.  NULL or
+ * not 8-byte aligned q_sums or k_sums is CHORUS_ERR_INVALID_ARG. */
 chorus_status chorus_build_block_mask_from_sums(const chorus_shape* shape, const double* q_sums,
                                                 const double* k_sums, double sm_scale, double top_p,
                                                 double min_top_k, int32_t kv_block, int32_t* row_ptr,
@@ -295,8 +295,8 @@ chorus_status chorus_quantize_fp8_blockwise(chorus_dtype in_dtype, const chorus_
  * codes and scales are bitwise those of chorus_quantize_fp8_blockwise.
  * block_sums : out, device float64 [B, H, n_blocks, 128], contiguous.
  * key_scale  : optional (NULL for none); same checks as the builder's.
- * Errors as chorus_quantize_fp8_blockwise; NULL block_sums is
- * CHORUS_ERR_INVALID_ARG. */
+ * Errors as chorus_quantize_fp8_blockwise; NULL or not 8-byte aligned
+ * block_sums is CHORUS_ERR_INVALID_ARG. */
 chorus_status chorus_quantize_fp8_blockwise_sums(chorus_dtype in_dtype, const chorus_shape* shape,
                                                  const chorus_tensor* x, const chorus_tensor* codes,
                                                  float* scales, const chorus_key_scale* key_scale,

@@ -282,6 +282,8 @@ chorus_status chorus_build_block_mask_from_sums(const chorus_shape* shape, const
   chorus_status st;
   if ((st = check_shape(shape))) return st;
   if (!q_sums || !k_sums) return fail(CHORUS_ERR_INVALID_ARG, "q_sums/k_sums is NULL");
+  if (reinterpret_cast<uintptr_t>(q_sums) % 8 || reinterpret_cast<uintptr_t>(k_sums) % 8)
+    return fail(CHORUS_ERR_INVALID_ARG, "q_sums/k_sums is not 8-byte aligned");
   int nk = 0, k_min = 0;
   if ((st = check_selection(shape, sm_scale, top_p, min_top_k, kv_block, row_ptr, col_idx, col_capacity, &nk,
                             &k_min)))
@@ -386,6 +388,8 @@ chorus_status chorus_quantize_fp8_blockwise_sums(chorus_dtype in_dtype, const ch
   if ((st = check_tensor(x, "x", 2))) return st;
   if ((st = check_tensor(codes, "codes", 1))) return st;
   if (!scales || !block_sums) return fail(CHORUS_ERR_INVALID_ARG, "scales/block_sums is NULL");
+  if (reinterpret_cast<uintptr_t>(block_sums) % 8)
+    return fail(CHORUS_ERR_INVALID_ARG, "block_sums is not 8-byte aligned");
   KeyScale ks;
   if ((st = check_key_scale(key_scale, shape->S, &ks))) return st;
   return from_hip(launch_quant_fp8(in_dtype, targ(x), targ(codes), shape->B, shape->S, shape->H, scales, ks,

@@ -151,6 +151,7 @@ def test_block_sums_entry_points_check_arguments(lib):
     assert q(ops.FP8_E4M3, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), FAKE, None, FAKE, None) == 2
     assert q(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), FAKE, None, None, None) == 1
     assert q(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), None, None, FAKE, None) == 1
+    assert q(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), FAKE, None, FAKE + 4, None) == 1
     assert q(ops.BF16, ctypes.byref(shp), ctypes.byref(t), ctypes.byref(t), FAKE, ctypes.byref(ks_bad), FAKE,
              None) == 1
     assert q(ops.BF16, ctypes.byref(shape(D=64)), ctypes.byref(t), ctypes.byref(t), FAKE, None, FAKE, None) == 2
@@ -164,6 +165,7 @@ def test_block_sums_entry_points_check_arguments(lib):
 
     assert call(qs=None) == 1
     assert call(kss=None) == 1
+    assert call(qs=FAKE + 4) == 1
     assert call(top_p=1.5) == 1
     assert call(mk=-0.1) == 1
     assert call(kvb=96) == 2
