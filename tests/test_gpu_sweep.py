@@ -56,6 +56,31 @@ def test_quantizer_lengths(S):
     oc, os_ = of.quantize_blockwise(np64(q))
     assert np.array_equal(codes.cpu().numpy(), oc)
     assert np.array_equal(scales.cpu().numpy(), os_)
+    # the variant with block sums: the same codes and scales, and sums / valid
+    # count equal to the oracle's block means
+    c2, s2, sums = ops.quantize_fp8_blockwise_sums(q.cuda())
+    torch.cuda.synchronize()
+    assert torch.equal(c2, codes) and torch.equal(s2.view(torch.int32), scales.view(torch.int32))
+    cnt = np.array([min(64, S - 64 * i) for i in range((S + 63) // 64)], dtype=np.float64)
+    means = sums.cpu().numpy() / cnt[None, None, :, None]
+    for h in range(q.shape[2]):
+        assert np.array_equal(means[0, h], om.pool_means(np64(q)[0, :, h]))
+
+
+@pytest.mark.parametrize("kv_block", [64, 128])
+@pytest.mark.parametrize("S", LENGTHS)
+def test_builder_from_block_sums_lengths(S, kv_block):
+    """The builder from the quantiser's block sums gives bitwise the mask of
+    the builder reading the same bf16 Q and K at every length."""
+    q, k, _ = qkv(S, torch.bfloat16, 3 * S + 1)
+    q, k = q.cuda(), k.cuda()
+    _, _, qs = ops.quantize_fp8_blockwise_sums(q)
+    _, _, kss = ops.quantize_fp8_blockwise_sums(k)
+    m = ops.build_block_mask_from_sums(qs, kss, S, 0.7, 0.1, sm_scale=SM, kv_block=kv_block)
+    ref = ops.build_block_mask(q, k, 0.7, 0.1, sm_scale=SM, kv_block=kv_block)
+    rp, ci = m.to_host()
+    rrp, rci = ref.to_host()
+    assert np.array_equal(rp, rrp) and np.array_equal(ci, rci), S
 
 
 @pytest.mark.parametrize("kv_block", [64, 128])
