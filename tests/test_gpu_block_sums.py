@@ -137,3 +137,18 @@ def test_block_sums_full_size_720p_14b():
         assert m.nnz == ref.nnz
         assert torch.equal(m.row_ptr, ref.row_ptr)
         assert torch.equal(m.col_idx[:m.nnz], ref.col_idx[:ref.nnz])
+
+
+def test_block_sums_of_strided_views():
+    """Batch- and head-sliced views of a larger tensor (token rows H_full * 128
+    apart) give bitwise the codes, scales and block sums of their contiguous
+    copies."""
+    x = rand_x(77, 3, 1000, 5, torch.bfloat16).cuda()
+    for view in (x[1:2], x[:, :, 1:4], x[2:3, :, 4:5]):
+        assert not view.is_contiguous() or view.data_ptr() != x.data_ptr()
+        c1, s1, t1 = ops.quantize_fp8_blockwise_sums(view, key_scale=(300, 1.25))
+        c2, s2, t2 = ops.quantize_fp8_blockwise_sums(view.contiguous(), key_scale=(300, 1.25))
+        torch.cuda.synchronize()
+        assert torch.equal(c1, c2)
+        assert torch.equal(s1.view(torch.int32), s2.view(torch.int32))
+        assert torch.equal(t1.view(torch.int64), t2.view(torch.int64))
