@@ -643,10 +643,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const void* __restr
 
 // Same selection with one wave per row for rows of at most 64 * kWaveMaxPer
 // blocks: lane l keeps the keys and masses of blocks l + 64 e in registers,
-// reductions are wave shuffles, the per-digit histogram lives in the wave's
-// own LDS slice, and the kept set is written as ballots (block 64 e + l is
-// bit l of word pair 2e, 2e + 1).  No workgroup barrier is needed; four rows
-// share a workgroup.
+// reductions are DPP / permlane steps and broadcasts are lane reads (no LDS
+// round trips), the per-digit histogram lives in the wave's own LDS slice,
+// and the kept set is written as ballots (block 64 e + l is bit l of word
+// pair 2e, 2e + 1).  No workgroup barrier is needed; four rows share a
+// workgroup.  Rows of 1,025-1,280 blocks (PER = 20) run at three waves per
+// SIMD: the 168-register cap spills a few registers, and the extra wave per
+// SIMD still makes the kernel faster than two unspilled waves.
 // ---------------------------------------------------------------------------
 constexpr int kWaveMaxPer = 32;   // n <= 2048
 
@@ -658,13 +661,83 @@ __device__ inline void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Value of lane src (wave-uniform; a negative src, from an empty ballot,
+// reads lane 0 and the caller ignores the result) at every lane.
 template <typename T>
 __device__ inline T wave_bcast(T v, int src) {
-  return __shfl(v, src);
+  const int s = src < 0 ? 0 : src;
+  if constexpr (sizeof(T) == 4) {
+    return __builtin_bit_cast(T, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), s));
+  } else {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, s);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), s);
+    return __builtin_bit_cast(T, (uint64_t)lo | ((uint64_t)hi << 32));
+  }
 }
 
+// Wave-wide reductions without the LDS crossbar that __shfl_xor goes
+// through: DPP moves inside each row of 16 lanes (quad lanes xor 1 and xor 2,
+// then the half-row mirror and the row mirror, each pairing two partial
+// results), then the permlane swaps of rows 2r / 2r + 1 and of the two
+// halves of the wave.  Each step combines the same two partial values at
+// every lane it reaches, so for a commutative op all lanes end with one
+// bitwise-identical result.
+template <int CTRL>
+__device__ inline uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL, typename T>
+__device__ inline T dpp_of(T v) {
+  if constexpr (sizeof(T) == 4) {
+    return __builtin_bit_cast(T, dpp_u32<CTRL>(__builtin_bit_cast(uint32_t, v)));
+  } else {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint64_t lo = dpp_u32<CTRL>((uint32_t)u), hi = dpp_u32<CTRL>((uint32_t)(u >> 32));
+    return __builtin_bit_cast(T, lo | (hi << 32));
+  }
+}
+// a, b = the value of the lower and of the upper row of a pair of rows
+// (HALVES: of the two halves of the wave), at every lane of both
+template <bool HALVES, typename T>
+__device__ inline void swap_pair(T v, T& a, T& b) {
+  if constexpr (sizeof(T) == 4) {
+    const uint32_t u = __builtin_bit_cast(uint32_t, v);
+    const auto r = HALVES ? __builtin_amdgcn_permlane32_swap(u, u, false, false)
+                          : __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    a = __builtin_bit_cast(T, (uint32_t)r[0]);
+    b = __builtin_bit_cast(T, (uint32_t)r[1]);
+  } else {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)u, hi = (uint32_t)(u >> 32);
+    const auto rl = HALVES ? __builtin_amdgcn_permlane32_swap(lo, lo, false, false)
+                           : __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto rh = HALVES ? __builtin_amdgcn_permlane32_swap(hi, hi, false, false)
+                           : __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    a = __builtin_bit_cast(T, (uint64_t)(uint32_t)rl[0] | ((uint64_t)(uint32_t)rh[0] << 32));
+    b = __builtin_bit_cast(T, (uint64_t)(uint32_t)rl[1] | ((uint64_t)(uint32_t)rh[1] << 32));
+  }
+}
+template <typename T, class Op>
+__device__ inline T wave_reduce(T v, Op op) {
+  v = op(v, dpp_of<0xB1>(v));    // quad_perm [1, 0, 3, 2]
+  v = op(v, dpp_of<0x4E>(v));    // quad_perm [2, 3, 0, 1]
+  v = op(v, dpp_of<0x141>(v));   // row_half_mirror
+  v = op(v, dpp_of<0x140>(v));   // row_mirror
+  T a, b;
+  swap_pair<false>(v, a, b);
+  v = op(a, b);
+  swap_pair<true>(v, a, b);
+  return op(a, b);
+}
+struct OpMax { template <typename T> __device__ T operator()(T a, T b) const { return a > b ? a : b; } };
+struct OpMin { template <typename T> __device__ T operator()(T a, T b) const { return a < b ? a : b; } };
+struct OpAdd { template <typename T> __device__ T operator()(T a, T b) const { return a + b; } };
+struct OpFMax { __device__ double operator()(double a, double b) const { return fmax(a, b); } };
+struct OpFMin { __device__ double operator()(double a, double b) const { return fmin(a, b); } };
+
 template <int PER, bool FROM_MASS>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ? 4 : PER <= 24 ? 2 : 1))) void select_wave_kernel(const void* __restrict__ in, int n, int64_t rows,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ? 4 : PER <= 20 ? 3 : PER <= 24 ? 2 : 1))) void select_wave_kernel(const void* __restrict__ in, int n, int64_t rows,
                                                           double top_p, int k_min, int32_t* __restrict__ counts,
                                                           uint32_t* __restrict__ bitmap, int words) {
   __shared__ uint32_t hist_cnt_all[4][256];
@@ -693,10 +766,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
     m = fmax(m, v);
     if (j < n) mn = fmin(mn, v);
   }
-  for (int o = 32; o > 0; o >>= 1) {
-    m = fmax(m, __shfl_xor(m, o));
-    mn = fmin(mn, __shfl_xor(mn, o));
-  }
+  m = wave_reduce(m, OpFMax());
+  mn = wave_reduce(mn, OpFMin());
   // value bins: floor((v - min) * 255.5 / (max - min)), non-decreasing in v,
   // so every block of a higher bin comes before every block of a lower one
   const double bscale = m > mn ? 255.5 / (m - mn) : 0.0;
@@ -717,7 +788,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
     }
     key[e] = j < n ? order_key(v) : 0;
   }
-  for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o);
+  z = wave_reduce(z, OpAdd());
   // block masses as 62-bit fixed point: round(x * 2^62 / z)
   const double to_fixed = z > 0.0 ? kMassOne / z : 0.0;
   uint64_t total = 0;
@@ -727,7 +798,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
     mass[e] = j < n ? __double2ull_rn(__longlong_as_double((long long)mass[e]) * to_fixed) : 0;
     total += mass[e];
   }
-  for (int o = 32; o > 0; o >>= 1) total += __shfl_xor(total, o);
+  total = wave_reduce(total, OpAdd());
 
   SelCond cond;
   cond.any_mass = !(top_p > 0.0);
@@ -844,10 +915,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
       wave_lds_sync();
       const bool ok = mine && cond(cnt_b + rank + 1, mass_b + cum + my_m);
       uint32_t r_min = ok ? rank : 0xffffffffu;
-      for (int o = 32; o > 0; o >>= 1) {
-        const uint32_t w = __shfl_xor(r_min, o);
-        r_min = w < r_min ? w : r_min;
-      }
+      r_min = wave_reduce(r_min, OpMin());
       const int src2 = __ffsll((long long)__builtin_amdgcn_ballot_w64(ok && rank == r_min)) - 1;
       if (src2 >= 0) {
         kb = wave_bcast(my_k, src2);
@@ -869,11 +937,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
         kmax = key[e] > kmax ? key[e] : kmax;
       }
     }
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint64_t a = __shfl_xor(kmin, o), b = __shfl_xor(kmax, o);
-      kmin = a < kmin ? a : kmin;
-      kmax = b > kmax ? b : kmax;
-    }
+    kmin = wave_reduce(kmin, OpMin());
+    kmax = wave_reduce(kmax, OpMax());
     const uint64_t diff = kmin ^ kmax;
     int lo = diff ? 64 - __clzll((long long)diff) : 0;
     uint64_t prefix = lo == 64 ? 0 : (kmin >> lo) << lo;
@@ -895,10 +960,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
           const int d = (int)((key[e] >> shift) & 255);
           if (j < n && (lo == 64 || ((key[e] ^ prefix) >> lo) == 0) && d < dig_limit) dmax = d > dmax ? d : dmax;
         }
-        for (int o = 32; o > 0; o >>= 1) {
-          const int w = __shfl_xor(dmax, o);
-          dmax = w > dmax ? w : dmax;
-        }
+        dmax = wave_reduce(dmax, OpMax());
         if (dmax < 0) break;
         uint32_t c = 0;
         uint64_t m = 0;
@@ -910,10 +972,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PER <= 16 ?
             m += mass[e];
           }
         }
-        for (int o = 32; o > 0; o >>= 1) {
-          c += __shfl_xor(c, o);
-          m += __shfl_xor(m, o);
-        }
+        c = wave_reduce(c, OpAdd());
+        m = wave_reduce(m, OpAdd());
         if (cond(cnt_above + c, mass_above + m)) {
           // the boundary block has this digit
           prefix = (prefix & ~(255ull << shift)) | ((uint64_t)dmax << shift);
