@@ -175,6 +175,23 @@ def test_block_sums_entry_points_check_arguments(lib):
     assert call(wsb=need - 1) == 5
 
 
+def test_block_sums_binding_checks_shapes_on_the_host(lib):
+    """The Python binding of the builder from block sums rejects mismatched
+    or mis-sized sums before any device call (CPU tensors suffice)."""
+    import torch
+    qs = torch.zeros((1, 2, 16, 128), dtype=torch.float64)
+    with pytest.raises(ValueError):
+        ops.build_block_mask_from_sums(qs, torch.zeros((1, 2, 15, 128), dtype=torch.float64), 1000, 0.5, 0.1)
+    with pytest.raises(ValueError):
+        ops.build_block_mask_from_sums(qs, qs.float(), 1000, 0.5, 0.1)
+    with pytest.raises(ValueError):   # S = 1000 has 16 blocks of 64 tokens, not 15
+        short = torch.zeros((1, 2, 15, 128), dtype=torch.float64)
+        ops.build_block_mask_from_sums(short, short, 1000, 0.5, 0.1)
+    with pytest.raises(ValueError):
+        ops.quantize_fp8_blockwise_sums(torch.zeros((1, 100, 2, 128), dtype=torch.bfloat16),
+                                        block_sums=torch.zeros((1, 2, 1, 128), dtype=torch.float64))
+
+
 def test_block_mass_selection_and_coverage_check_arguments(lib):
     shp = shape(B=1, S=100, H=2)
     t = t4()
